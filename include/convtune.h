@@ -1,0 +1,271 @@
+/*
+ * convtune.h -- C ABI of the MI355X conv2d tuning library (libconvtune.so).
+ *
+ * The library implements the measurement side of the paper's autotuning loop
+ * (section 2.1, Fig. 1a: select candidate configurations, build, profile on
+ * the target device, search) for one DNN operator, conv2d, on gfx950:
+ *
+ *   - a schedule-parametrised conv2d kernel family (direct and depthwise fp32
+ *     on the vector ALU, implicit GEMM on MFMA in fp32 and bf16);
+ *   - "profile": run a candidate on a stream restricted to a fixed share of
+ *     the compute units and time it with HIP events (section 2.2: a fixed GPU
+ *     share per profiling process isolates it and gives predictable latency;
+ *     here the share is a CU mask, hipExtStreamCreateWithCUMask);
+ *   - several tuning clients at once on disjoint CU shares (section 3.1.1:
+ *     profiling servers with distinct GPU shares, and the operators of a model
+ *     sharded over tuning clients);
+ *   - cross-evaluation: a schedule tuned at one share re-run at another
+ *     (section 2.2.1, Tables 1 and 2).
+ *
+ * Conventions for every entry point:
+ *   - All functions are extern "C", thread-safe, and never throw.
+ *   - Return value: 0 on success, or a negative CT_E_* code; the message of
+ *     the last failure on the calling thread is in ct_last_error().
+ *   - Device pointers (x, w, y, references) are caller-owned HIP device
+ *     memory, contiguous, in the layout and dtype that ct_op states. The
+ *     library never frees caller memory; it owns its streams, events and
+ *     split-reduction workspaces and releases them in ct_shutdown().
+ *   - Host arrays (latencies, status, masks, schedules) are caller-owned.
+ *   - Calls from different threads run concurrently on different HIP streams;
+ *     two threads with the same CU mask still get separate streams.
+ *
+ * Operator (the reading of conv2d used throughout, since the paper names the
+ * operator but does not write it out): cross-correlation with zero padding,
+ * floor output size and grouped channels,
+ *   OH = floor((H + 2 ph - dh (R-1) - 1) / sh) + 1,
+ *   y[n,k,p,q] = sum_{c<C/g, r<R, t<S} x[n, (k div K/g) C/g + c, p sh - ph + r dh,
+ *                                       q sw - pw + t dw] * w[k,c,r,t].
+ */
+#ifndef CONVTUNE_H
+#define CONVTUNE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes (return values) ---- */
+#define CT_OK          0
+#define CT_E_ARG      -1   /* bad argument: null pointer, bad shape, bad size   */
+#define CT_E_HIP      -2   /* a HIP call failed; its message is in ct_last_error */
+#define CT_E_NOINIT   -3   /* ct_init() has not succeeded                        */
+#define CT_E_OOM      -4   /* workspace allocation failed                        */
+#define CT_E_NODEV    -5   /* no usable gfx950 device                            */
+
+/* ---- per-candidate status codes (status[] outputs) ---- */
+#define CT_S_OK           0
+#define CT_S_INVALID      1  /* rejected by the validator; never launched, latency +inf */
+#define CT_S_LAUNCH       2  /* the launch itself failed                                */
+#define CT_S_TIMEOUT      3  /* measured latency above the protocol's time limit        */
+#define CT_S_WRONG_ANSWER 4  /* output differs from the reference beyond tolerance      */
+
+/* ---- kernel families ---- */
+#define CT_FAM_DIRECT_F32     1  /* NCHW fp32, groups 1, vector-ALU direct convolution       */
+#define CT_FAM_DEPTHWISE_F32  2  /* NCHW fp32, groups = C = K, vector-ALU depthwise           */
+#define CT_FAM_IGEMM_BF16     3  /* NHWC bf16 in, fp32 out, 1x1 stride 1: MFMA implicit GEMM  */
+#define CT_FAM_IGEMM_F32      4  /* NCHW fp32, groups 1, any filter: fp32 MFMA implicit GEMM  */
+#define CT_NUM_FAMILIES       4
+
+#define CT_DT_F32   0
+#define CT_DT_BF16  1
+#define CT_LAYOUT_NCHW 0  /* x N,C,H,W; w K,C/g,R,S; y N,K,OH,OW                 */
+#define CT_LAYOUT_NHWC 1  /* x N,H,W,C; w K,R,S,C/g (K,C for 1x1); y N,OH,OW,K   */
+
+#define CT_MASK_WORDS 8   /* CU masks are 8 x 32 bits: bit i of word j = CU 32 j + i */
+#define CT_MAX_KNOBS  15
+
+/* One conv2d task (the paper's tuning task: one operator at one shape). */
+typedef struct ct_op {
+    int32_t n, c, h, w, k, r, s;
+    int32_t stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, groups;
+    int32_t dtype;   /* CT_DT_*; x and w in this type, y always fp32 */
+    int32_t layout;  /* CT_LAYOUT_* */
+} ct_op;
+
+/* One candidate configuration (the paper's "configuration": tiles, loop
+ * order, caching in LDS, unrolling, threading, matrix units -- section 2.1).
+ * knob[] holds the family's knob values in its documented order; unused
+ * slots are 0. Use ct_grid_decode to obtain valid encodings. */
+typedef struct ct_schedule {
+    int32_t family;
+    int32_t knob[CT_MAX_KNOBS];
+} ct_schedule;
+
+/* Timing protocol. Each candidate: `warmup` untimed runs, then `repeats`
+ * repeats of (event record; `launches` back-to-back runs; event record).
+ * Latency = median over repeats of (elapsed / launches). Candidates are
+ * enqueued in groups of `batch` with one stream synchronisation per group.
+ * A candidate whose latency exceeds timeout_ms gets CT_S_TIMEOUT. */
+typedef struct ct_measure_opts {
+    int32_t warmup;
+    int32_t repeats;     /* 1..64 */
+    int32_t launches;    /* >= 1  */
+    int32_t batch;       /* >= 1; candidates per synchronisation */
+    float   timeout_ms;
+    int32_t interleave;  /* 1: repeats run round-robin across the candidates */
+} ct_measure_opts;
+
+/* Optional correctness check during measurement: after each candidate's
+ * last timed run, the device compares y with y_ref (fp32, same layout as y)
+ * and sets CT_S_WRONG_ANSWER when max|y - y_ref| > tol * max|y_ref|. */
+typedef struct ct_verify {
+    const float *y_ref;  /* device pointer, or NULL for no check */
+    float tol;
+} ct_verify;
+
+/* ---- set-up and device facts ---- */
+
+/* Select HIP device `device`, check that it is gfx950, read its CU count and
+ * build the per-process state. Idempotent for the same device. */
+int ct_init(int device);
+/* Compute units of the initialised device (256 on MI355X), or CT_E_NOINIT. */
+int ct_num_cus(void);
+/* Release streams, events and workspaces of every thread. */
+void ct_shutdown(void);
+/* Message of the last failure on the calling thread ("" if none). The
+ * pointer stays valid until the thread's next library call. */
+const char *ct_last_error(void);
+
+/* ---- CU masks (section 2.2: a fixed share of the device per process) ---- */
+
+/* Mask for `slot` of the share `fraction` on a device with num_cus CUs:
+ * m = round(num_cus * fraction) CUs, slot j = bits [j m, (j+1) m). A
+ * contiguous bit block spreads evenly over the XCDs because the driver
+ * deals consecutive mask bits out to the XCDs in turn. Pure host function.
+ * Returns CT_E_ARG if m = 0, words < num_cus/32, or the slot does not fit. */
+int ct_build_cu_mask(int num_cus, double fraction, int slot, uint32_t *mask, int words);
+/* Same, for the initialised device. */
+int ct_cu_mask(double fraction, int slot, uint32_t *mask, int words);
+
+/* ---- knob grids and validation (host only) ---- */
+
+/* Number of knobs of a family and the raw grid size (product of the value
+ * counts). */
+int ct_grid_info(int family, int32_t *num_knobs, int64_t *grid_size);
+/* Value list of knob `knob` of `family`: writes up to cap values, sets *count. */
+int ct_knob_values(int family, int knob, int32_t *values, int32_t cap, int32_t *count);
+/* Mixed-radix decode/encode: the first knob is the most significant digit. */
+int ct_grid_decode(int family, int64_t index, ct_schedule *out);
+int ct_grid_encode(const ct_schedule *s, int64_t *index);
+/* 0 if schedule s may run on op, CT_S_INVALID if the validator rejects it
+ * (reason in ct_last_error), CT_E_ARG for a malformed op or schedule.
+ * Every schedule that passes is safe to launch: all its global accesses are
+ * bounds-checked and its LDS, thread and grid sizes fit the device. */
+int ct_validate(const ct_op *op, const ct_schedule *s);
+/* LDS bytes, threads per block and blocks of one run of s on op (for
+ * reports); the schedule must be valid. */
+int ct_launch_shape(const ct_op *op, const ct_schedule *s, int32_t *lds_bytes,
+                    int32_t *threads, int64_t *blocks, int32_t *kernels);
+
+/* ---- candidate generation (section 2.1 stage 1: with no history, pick
+ *      random candidates from the search space) ---- */
+
+/* The candidate space of op is the concatenation, in ascending family order,
+ * of each applicable family's valid grid indices in ascending order. Writes
+ * up to cap schedules of it in that order; *count = its full size. */
+int ct_valid_space(const ct_op *op, ct_schedule *out, int64_t cap, int64_t *count);
+/* Seeded sample of n candidates without replacement: a partial Fisher-Yates
+ * shuffle of the candidate space driven by splitmix64 from state
+ *   seed ^ (0x9E3779B97F4A7C15 * (1 + config_id)) ^ (0xC0FFEE << 32) ^ layer_id
+ * (first output discarded): for i < n, j = i + next() mod (|V| - i), swap.
+ * out[i] is the candidate at sample position i. If |V| < n, all |V| are
+ * returned (in shuffled order). *n_out = number written. */
+int ct_sample(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_id,
+              int32_t n, ct_schedule *out, int32_t *n_out);
+
+/* ---- running and timing (section 2.1 stage 3, "profile") ---- */
+
+/* Run schedule s once on op: y = conv2d(x, w). cu_mask = NULL uses all CUs.
+ * Returns after the run has completed. CT_E_ARG if s is invalid for op. */
+int conv2d_run(const ct_op *op, const ct_schedule *s, const void *x, const void *w, void *y,
+               const uint32_t *cu_mask, int words);
+
+/* Time n candidates on slot 0 of the share cu_fraction, with the protocol o.
+ * lat_us[i] = median latency in microseconds (+inf unless status OK),
+ * status[i] = CT_S_*. rep_us (optional, n * o->repeats) receives every
+ * repeat's per-run time. y is overwritten. Returns 0 even if some
+ * candidates fail; a negative code means the call itself failed. */
+int measure_candidates(const ct_op *op, const ct_schedule *s, int n, double cu_fraction,
+                       const ct_measure_opts *o, const void *x, const void *w, void *y,
+                       float *lat_us, int32_t *status);
+/* Same with an explicit CU mask, optional verification and repeat output. */
+int measure_candidates_mask(const ct_op *op, const ct_schedule *s, int n,
+                            const uint32_t *cu_mask, int words, const ct_measure_opts *o,
+                            const ct_verify *v, const void *x, const void *w, void *y,
+                            float *lat_us, int32_t *status, float *rep_us);
+
+/* ---- selection (stage 4 of the loop; the best configuration is the one
+ *      with the lowest measured latency, as the early-stop rule implies) ---- */
+
+/* Order of stage-1 screening: indices of the t fastest OK candidates, by
+ * (latency, sample position) ascending. Writes min(t, #OK) indices. */
+int ct_top_t(const float *lat_us, const int32_t *status, int n, int t, int32_t *top, int32_t *n_top);
+/* Winner among the re-measured candidates: the lowest sample position among
+ * those whose latency is within (1 + eps) of the minimum. pos[i] is the sample
+ * position of candidate i. Returns the index i of the winner in *winner. */
+int ct_select_winner(const float *lat_us, const int32_t *pos, int n, float eps, int32_t *winner);
+
+/* ---- tuning clients (section 3.1.1) ---- */
+
+/* One layer to tune: the candidate list (in sample order), its buffers and
+ * the result fields the library fills. */
+typedef struct ct_tune_job {
+    ct_op op;
+    const void *x, *w;  void *y;        /* device buffers for this layer       */
+    const ct_schedule *cands;  int32_t n_cands;
+    ct_verify verify;                   /* optional correctness check          */
+    /* outputs */
+    float   *lat1_us;  int32_t *status1; /* caller arrays [n_cands]: screening  */
+    int32_t top_t;                       /* in: re-measure this many (>= 1)     */
+    int32_t *top_pos;  float *lat2_us;   /* caller arrays [top_t]: re-measure   */
+    int32_t n_top;                       /* out: entries used in top_pos/lat2   */
+    int32_t winner_pos;                  /* out: sample position of the winner, -1 if none */
+    float   winner_lat_us;               /* out */
+    double  t_start_s, t_end_s;          /* out: steady-clock seconds           */
+} ct_tune_job;
+
+/* One tuning client: a host thread that owns a CU-masked stream and tunes
+ * its jobs in order (screen all candidates, re-measure the top_t with the
+ * stage-2 protocol interleaved across them, select the winner). */
+typedef struct ct_client {
+    uint32_t cu_mask[CT_MASK_WORDS];
+    int32_t host_core;                   /* pin the thread to this core; -1 = no pinning */
+    ct_tune_job *jobs;  int32_t n_jobs;
+    int32_t rc;                          /* out: 0 or a CT_E_* code             */
+    double t_start_s, t_end_s;           /* out: first job start, last job end  */
+    int64_t n_measured;                  /* out: candidates screened            */
+} ct_client;
+
+/* Run n_clients clients concurrently, one host thread each, and wait for all.
+ * Clients with overlapping masks are allowed but then share CUs. */
+int ct_tune_clients(ct_client *clients, int n_clients, const ct_measure_opts *stage1,
+                    const ct_measure_opts *stage2, float eps);
+
+/* ---- cross-evaluation (section 2.2.1, Tables 1-2: tuned at f, run at g) ---- */
+
+/* M[i * n_masks + j] = stage-2 latency of schedule s[i] run on mask j. The
+ * repeats of all (i, j) cells are interleaved round-robin per mask. */
+int ct_cross_eval(const ct_op *op, const ct_schedule *s, int n_sched,
+                  const uint32_t *masks, int n_masks, int words,
+                  const ct_measure_opts *o, const void *x, const void *w, void *y, float *M);
+
+/* ---- probes (support for masks and rooflines) ---- */
+
+/* Launch `blocks` one-wave blocks on the mask; each records the hardware
+ * (XCC, SE, SH, CU) of the CU it ran on. out[i] = packed id
+ * (xcc << 12 | se << 8 | sh << 4 | cu) of the i-th distinct CU seen,
+ * *n_out = number of distinct CUs (<= cap written). */
+int ct_probe_cus(const uint32_t *cu_mask, int words, int blocks, int32_t *out, int cap, int32_t *n_out);
+/* Median time per launch of an empty kernel with `blocks` blocks on the mask
+ * (the dispatch floor of the timing protocol). */
+int ct_probe_empty(const uint32_t *cu_mask, int words, int blocks, const ct_measure_opts *o, float *us);
+/* Achieved copy bandwidth (read + write bytes / time) of a bytes-sized
+ * device-to-device copy kernel on the mask, in GB/s. Buffers are the caller's. */
+int ct_probe_copy(const uint32_t *cu_mask, int words, const void *src, void *dst, int64_t bytes,
+                  const ct_measure_opts *o, float *gbps);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CONVTUNE_H */

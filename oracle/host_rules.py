@@ -1,0 +1,121 @@
+"""Oracle of the integer/host rules of the tuning loop -- TEST INFRASTRUCTURE ONLY.
+
+Plain Python, written from the stated definitions, sharing nothing with the
+library. Each function names the rule it follows.
+
+* Candidate selection with no history is random (paper, section 2.1, stage
+  "select configurations"). The rule fixed here: a partial Fisher-Yates
+  shuffle of the ascending valid candidate list, driven by splitmix64
+  (Steele, Lea, Flood, OOPSLA 2014), from state
+  seed ^ (GAMMA * (1 + config_id) mod 2^64) ^ (0xC0FFEE << 32) ^ layer_id,
+  first output discarded; j = i + next() mod (|V| - i).
+* A configuration's latency is the median of its repeats (the profile stage
+  measures execution time; the statistic is this build's reading).
+* The best configuration is the one with the lowest latency (implied by the
+  early-stop rule of section 2.2.1, which stops when new configurations no
+  longer lower it). Screening keeps the t fastest by (latency, sample position);
+  among the re-measured ones every latency within (1 + eps) of the minimum is
+  a tie and the lowest sample position wins.
+* A fixed GPU share per process (section 2.2) is a CU mask: m = round(n f) CUs,
+  slot j = mask bits [j m, (j + 1) m).
+* Knob grids are mixed-radix numbers, first knob most significant.
+"""
+from __future__ import annotations
+
+import math
+from typing import List, Sequence
+
+MASK64 = (1 << 64) - 1
+GAMMA = 0x9E3779B97F4A7C15
+
+
+class SplitMix64:
+    """splitmix64: state += GAMMA; z = state; two xor-shift-multiply rounds; final xor-shift."""
+
+    def __init__(self, state: int):
+        self.state = state & MASK64
+
+    def next(self) -> int:
+        self.state = (self.state + GAMMA) & MASK64
+        z = self.state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64
+        return z ^ (z >> 31)
+
+
+def sampler_state(seed: int, config_id: int, layer_id: int) -> int:
+    return (seed ^ ((GAMMA * (1 + config_id)) & MASK64) ^ ((0xC0FFEE << 32) & MASK64)
+            ^ (layer_id & 0xFFFFFFFF)) & MASK64
+
+
+def sample_positions(space_size: int, n: int, seed: int, config_id: int, layer_id: int) -> List[int]:
+    """Indices into the ascending valid list, in sample order (partial Fisher-Yates)."""
+    rng = SplitMix64(sampler_state(seed, config_id, layer_id))
+    rng.next()  # the first output is discarded
+    v = list(range(space_size))
+    out = []
+    for i in range(min(n, space_size)):
+        j = i + rng.next() % (space_size - i)
+        v[i], v[j] = v[j], v[i]
+        out.append(v[i])
+    return out
+
+
+def mixed_radix_decode(radices: Sequence[int], index: int) -> List[int]:
+    """Digits of index, first digit most significant."""
+    digits = []
+    for r in reversed(radices):
+        digits.append(index % r)
+        index //= r
+    return digits[::-1]
+
+
+def mixed_radix_encode(radices: Sequence[int], digits: Sequence[int]) -> int:
+    idx = 0
+    for r, d in zip(radices, digits):
+        idx = idx * r + d
+    return idx
+
+
+def cu_mask(num_cus: int, fraction: float, slot: int, words: int = 8) -> List[int]:
+    m = int(math.floor(num_cus * fraction + 0.5))
+    if m <= 0 or (slot + 1) * m > num_cus:
+        raise ValueError("slot does not fit")
+    bits = [0] * words
+    for b in range(slot * m, (slot + 1) * m):
+        bits[b // 32] |= 1 << (b % 32)
+    return bits
+
+
+def median(values) -> float:
+    """Median of float32 values; an even count averages the two middle ones in fp64."""
+    import numpy as np
+    v = sorted(float(np.float32(x)) for x in values)
+    n = len(v)
+    if n % 2:
+        return np.float32(v[n // 2])
+    return np.float32((v[n // 2 - 1] + v[n // 2]) / 2.0)
+
+
+def top_t(lat, status, t: int) -> List[int]:
+    ok = [i for i in range(len(lat)) if status[i] == 0 and math.isfinite(lat[i])]
+    ok.sort(key=lambda i: (float(lat[i]), i))
+    return ok[:t]
+
+
+def select_winner(lat, pos, eps: float) -> int:
+    """Index (into lat) of the winner, or -1 if no latency is finite."""
+    import numpy as np
+    finite = [float(l) for l in lat if math.isfinite(l)]
+    if not finite:
+        return -1
+    limit = min(finite) * (1.0 + float(np.float32(eps)))
+    tied = [i for i in range(len(lat)) if math.isfinite(lat[i]) and float(lat[i]) <= limit]
+    return min(tied, key=lambda i: pos[i])
+
+
+def xcd_swizzle(block: int, tiles: int, xcds: int = 8) -> int:
+    """Logical tile of a block when each XCD (blocks dealt round-robin) gets a contiguous range."""
+    q, r = divmod(tiles, xcds)
+    x, idx = block % xcds, block // xcds
+    return x * (q + 1) + idx if x < r else r * (q + 1) + (x - r) * q + idx

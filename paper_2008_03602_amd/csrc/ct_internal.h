@@ -1,0 +1,100 @@
+// Internal declarations of libconvtune: knob tables, derived op facts and the
+// launch geometry of each kernel family. The validator and the launchers both
+// derive a schedule's geometry from the functions declared here, so a
+// schedule that validates is launched exactly as it was checked.
+#pragma once
+
+#include <cstdint>
+#include <string>
+
+#include "convtune.h"
+
+namespace ct {
+
+constexpr int kMaxLdsBytes = 64 * 1024;   // per-block LDS budget of every schedule
+constexpr int kMaxThreads = 1024;
+constexpr int kMinThreads = 32;
+constexpr int kMaxLoadsPerThread = 8;     // register staging bound of the GEMM loaders
+
+// ---- derived facts of one op ----
+struct OpX {
+  ct_op op;
+  int64_t oh, ow;
+  int64_t cg, kg;
+  int64_t kred;        // Cg * R * S
+  int64_t npix;        // N * OH * OW
+  int64_t nx, nw, ny;  // element counts
+  int elem_bytes;      // of x and w
+};
+
+// Fills x from op; returns false (with a reason) if the op itself is malformed.
+bool derive_op(const ct_op& op, OpX* x, std::string* why);
+
+// ---- knob tables ----
+struct KnobDef {
+  const char* name;
+  int nvals;
+  int32_t vals[12];
+};
+struct FamilyDef {
+  int family;
+  const char* name;
+  int nknobs;
+  KnobDef knobs[CT_MAX_KNOBS];
+};
+const FamilyDef* family_def(int family);  // nullptr for an unknown family
+int64_t family_grid_size(const FamilyDef& f);
+
+// Which families apply to an op (layout, dtype and grouping contract).
+bool family_applies(int family, const OpX& x);
+
+// ---- per-family geometry ----
+// Knob positions of each family, in table order.
+namespace direct_knob { enum { TOH, TOW, TK, MK, MW, LDS, CT, SPLIT, UNR, COUNT }; }
+namespace dw_knob { enum { TC, TOH, TOW, VEC, RPT, LDS, NB, ORDER, COUNT }; }
+namespace bf16_knob { enum { MF, TM, TN, WM, WN, KC, LDS, SPLIT, SWZ, COUNT }; }
+namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, KC, STAGES, SPLIT, COUNT }; }
+
+// Filter/stride specialisation chosen from the op (not a knob).
+enum Spec { SPEC_GENERIC = 0, SPEC_1X1_S1 = 1, SPEC_1X1_S2 = 2, SPEC_3X3_S1 = 3, SPEC_3X3_S2 = 4 };
+Spec op_spec(const OpX& x);
+
+struct Geom {
+  int family;
+  Spec spec;
+  int threads;        // per block
+  int lds_bytes;      // dynamic LDS per block
+  int64_t blocks;     // main kernel
+  int split;          // >1: partial sums to workspace + reduction kernel
+  int kernels;        // launches per run (1 or 2)
+  int64_t ws_floats;  // workspace floats needed (split * ny)
+  // family-specific derived values
+  int64_t tiles_h, tiles_w, tiles_k, tiles_c, tiles_n;  // grid factors
+  int ih_t, iw_t;     // input halo tile (direct, depthwise)
+  int bm, bn;         // GEMM block tile (rows x cols)
+  int chunks;         // reduction chunks in total
+  int chunks_per_split;
+  int a_loads, b_loads;  // per-thread staged loads per chunk (GEMM families)
+};
+
+// Validates s on x and fills g. Returns CT_OK or CT_S_INVALID (reason in why).
+int compute_geom(const OpX& x, const ct_schedule& s, Geom* g, std::string* why);
+
+// ---- kernel launchers (one per family, in the .hip files) ----
+// ws: workspace of at least g.ws_floats floats when g.split > 1.
+int launch_direct_f32(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
+                      const void* w, void* y, float* ws, void* stream);
+int launch_depthwise_f32(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
+                         const void* w, void* y, float* ws, void* stream);
+int launch_igemm_bf16(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
+                      const void* w, void* y, float* ws, void* stream);
+int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
+                     const void* w, void* y, float* ws, void* stream);
+// Sums split partial outputs in split order: y[i] = sum_j ws[j * n + i].
+int launch_split_reduce(const float* ws, float* y, int64_t n, int split, void* stream);
+
+// ---- host rules shared by the C ABI ----
+void set_error(const std::string& msg);
+uint64_t splitmix64_next(uint64_t* state);
+
+}  // namespace ct

@@ -1,0 +1,194 @@
+#pragma once
+// Kernel template of family 1, DIRECT_F32, included by the per-MK units.
+// Family 1, DIRECT_F32: direct convolution on the vector ALU, NCHW x,
+// K x C x R x S w, NCHW y, fp32 throughout.
+//
+// A block computes a TK x TOH x TOW output tile of one image. Each thread
+// owns MK consecutive output channels and MW output columns of one row; the
+// MW columns are TOW/MW apart, so a wave's lanes touch consecutive columns
+// (coalesced global stores, conflict-free LDS reads). The reduction runs over
+// input-channel chunks of CT; with LDS staging the input halo tile and the
+// filter chunk are copied to LDS once per chunk and shared by the block.
+// SPLIT > 1 gives each split a contiguous channel range and writes partial
+// sums to a workspace that a second kernel adds in split order.
+//
+// Compile-time: MK, MW, LDS, UNR and the filter/stride specialisation
+// (generic, 1x1 s1/s2, 3x3 pad 1 s1/s2). Runtime: tiles, CT, SPLIT.
+// Every global access is bounds-checked against the tensor extents.
+#include <hip/hip_runtime.h>
+
+#include "ct_internal.h"
+
+namespace ct {
+
+struct DirectArgs {
+  int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
+  int OH, OW;
+  int toh, tow, tk, ct;
+  int tiles_w;
+  int split, cps;
+  int ih_t, iw_t;
+  int threads, tp, cols;
+  int64_t ny;
+};
+
+__host__ __device__ constexpr int spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
+__host__ __device__ constexpr int spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
+
+template <int MK, int MW, bool LDS, int SPEC, int UNR>
+__global__ void __launch_bounds__(1024)
+direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ out,
+                  DirectArgs a) {
+  constexpr int RC = spec_r(SPEC), STC = spec_stride(SPEC);
+  const int R = RC ? RC : a.R, S = RC ? RC : a.S;
+  const int sh = STC ? STC : a.sh, sw = STC ? STC : a.sw;
+  const int dh = SPEC ? 1 : a.dh, dw = SPEC ? 1 : a.dw;
+  const int ph = SPEC ? RC / 2 : a.ph, pw = SPEC ? RC / 2 : a.pw;
+  const int RS = R * S;
+  const int C = a.C, H = a.H, W = a.W, K = a.K;
+
+  extern __shared__ float smem[];
+  const int t = threadIdx.x;
+  const int th = blockIdx.x / a.tiles_w, tw = blockIdx.x - th * a.tiles_w;
+  const int k0 = blockIdx.y * a.tk;
+  const int n = blockIdx.z / a.split, sp = blockIdx.z - n * a.split;
+  const int oh0 = th * a.toh, ow0 = tw * a.tow;
+  const int tki = t / a.tp, tpi = t - tki * a.tp;
+  const int lr = tpi / a.cols, lc = tpi - lr * a.cols;
+  const int oh = oh0 + lr;
+  const int kbase = k0 + tki * MK;
+
+  float acc[MK][MW];
+#pragma unroll
+  for (int i = 0; i < MK; ++i)
+#pragma unroll
+    for (int j = 0; j < MW; ++j) acc[i][j] = 0.f;
+
+  const int c_begin = sp * a.cps * a.ct;
+  const int c_end = min(C, c_begin + a.cps * a.ct);
+  const int ih_org = oh0 * sh - ph, iw_org = ow0 * sw - pw;
+  const float* xn = x + (int64_t)n * C * H * W;
+
+  for (int cc = c_begin; cc < c_end; cc += a.ct) {
+    const int nc = min(a.ct, c_end - cc);
+    if constexpr (LDS) {
+      float* xs = smem;
+      float* wsm = smem + a.ct * a.ih_t * a.iw_t;
+      const int plane = a.ih_t * a.iw_t;
+      const int xt = a.ct * plane;
+      for (int e = t; e < xt; e += a.threads) {
+        const int c = e / plane;
+        const int rem = e - c * plane;
+        const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
+        const int gh = ih_org + hh, gw = iw_org + ww;
+        float v = 0.f;
+        if (c < nc && gh >= 0 && gh < H && gw >= 0 && gw < W) v = xn[((int64_t)(cc + c) * H + gh) * W + gw];
+        xs[e] = v;
+      }
+      const int crs = a.ct * RS;
+      const int wt = a.tk * crs;
+      for (int e = t; e < wt; e += a.threads) {
+        const int kk = e / crs;
+        const int rem = e - kk * crs;
+        const int c = rem / RS, rs = rem - c * RS;
+        float v = 0.f;
+        if (k0 + kk < K && c < nc) v = w[((int64_t)(k0 + kk) * C + cc + c) * RS + rs];
+        wsm[e] = v;
+      }
+      __syncthreads();
+#pragma unroll UNR
+      for (int c = 0; c < nc; ++c) {
+        const float* xr = xs + c * plane + (lr * sh) * a.iw_t + lc * sw;
+        const float* wr = wsm + (tki * MK * a.ct + c) * RS;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+#pragma unroll
+          for (int s = 0; s < S; ++s) {
+            float xv[MW], wv[MK];
+#pragma unroll
+            for (int j = 0; j < MW; ++j) xv[j] = xr[(r * dh) * a.iw_t + j * a.cols * sw + s * dw];
+#pragma unroll
+            for (int i = 0; i < MK; ++i) wv[i] = wr[i * a.ct * RS + r * S + s];
+#pragma unroll
+            for (int i = 0; i < MK; ++i)
+#pragma unroll
+              for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+          }
+        }
+      }
+      __syncthreads();
+    } else {
+#pragma unroll UNR
+      for (int c = 0; c < nc; ++c) {
+        const float* xc = xn + (int64_t)(cc + c) * H * W;
+        for (int r = 0; r < R; ++r) {
+          const int gh = oh * sh - ph + r * dh;
+          const bool hok = gh >= 0 && gh < H && oh < a.OH;
+          for (int s = 0; s < S; ++s) {
+            float xv[MW], wv[MK];
+#pragma unroll
+            for (int j = 0; j < MW; ++j) {
+              const int ow = ow0 + lc + j * a.cols;
+              const int gw = ow * sw - pw + s * dw;
+              xv[j] = (hok && gw >= 0 && gw < W) ? xc[(int64_t)gh * W + gw] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < MK; ++i) {
+              const int k = kbase + i;
+              wv[i] = k < K ? w[((int64_t)k * C + cc + c) * RS + r * S + s] : 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < MK; ++i)
+#pragma unroll
+              for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+          }
+        }
+      }
+    }
+  }
+
+  if (oh >= a.OH) return;
+  float* o = out + (int64_t)sp * a.ny;
+#pragma unroll
+  for (int i = 0; i < MK; ++i) {
+    const int k = kbase + i;
+    if (k >= K) break;
+#pragma unroll
+    for (int j = 0; j < MW; ++j) {
+      const int ow = ow0 + lc + j * a.cols;
+      if (ow < a.OW) o[(((int64_t)n * K + k) * a.OH + oh) * a.OW + ow] = acc[i][j];
+    }
+  }
+}
+
+using DirectFn = void (*)(const float*, const float*, float*, DirectArgs);
+
+
+template <int MK, int MW, bool LDS, int SPEC>
+static DirectFn pick_unr(int unr) {
+  return unr == 2 ? (DirectFn)direct_f32_kernel<MK, MW, LDS, SPEC, 2>
+                  : (DirectFn)direct_f32_kernel<MK, MW, LDS, SPEC, 1>;
+}
+template <int MK, int MW, bool LDS>
+static DirectFn pick_spec(int spec, int unr) {
+  switch (spec) {
+    case SPEC_1X1_S1: return pick_unr<MK, MW, LDS, 1>(unr);
+    case SPEC_1X1_S2: return pick_unr<MK, MW, LDS, 2>(unr);
+    case SPEC_3X3_S1: return pick_unr<MK, MW, LDS, 3>(unr);
+    case SPEC_3X3_S2: return pick_unr<MK, MW, LDS, 4>(unr);
+    default: return pick_unr<MK, MW, LDS, 0>(unr);
+  }
+}
+template <int MK, int MW>
+static DirectFn pick_lds(int lds, int spec, int unr) {
+  return lds ? pick_spec<MK, MW, true>(spec, unr) : pick_spec<MK, MW, false>(spec, unr);
+}
+template <int MK>
+DirectFn pick_mw(int mw, int lds, int spec, int unr) {
+  switch (mw) {
+    case 1: return pick_lds<MK, 1>(lds, spec, unr);
+    case 2: return pick_lds<MK, 2>(lds, spec, unr);
+    default: return pick_lds<MK, 4>(lds, spec, unr);
+  }
+}
+}  // namespace ct

@@ -1,0 +1,6 @@
+// Instantiations of family 1 (DIRECT_F32) with MK = 8 output channels per thread.
+#include "k_direct.inc.h"
+
+namespace ct {
+DirectFn pick_direct_mk8(int mw, int lds, int spec, int unr) { return pick_mw<8>(mw, lds, spec, unr); }
+}  // namespace ct

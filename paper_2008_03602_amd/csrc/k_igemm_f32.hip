@@ -1,0 +1,50 @@
+// Family 4, IGEMM_F32: launcher. The kernel and its description are in
+// k_igemm_f32.inc.h; the instantiations live in one unit per MFMA shape.
+#include "k_igemm_f32.inc.h"
+
+namespace ct {
+
+IgF32Fn igf32_pick_mf16_tm1(int tn, int stages, int spec);
+IgF32Fn igf32_pick_mf16_tm2(int tn, int stages, int spec);
+IgF32Fn igf32_pick_mf16_tm4(int tn, int stages, int spec);
+IgF32Fn igf32_pick_mf32_tm1(int tn, int stages, int spec);
+IgF32Fn igf32_pick_mf32_tm2(int tn, int stages, int spec);
+IgF32Fn igf32_pick_mf32_tm4(int tn, int stages, int spec);
+
+static IgF32Fn igf32_pick(int mf, int tm, int tn, int stages, int spec) {
+  if (mf == 32) {
+    if (tm == 1) return igf32_pick_mf32_tm1(tn, stages, spec);
+    if (tm == 2) return igf32_pick_mf32_tm2(tn, stages, spec);
+    return igf32_pick_mf32_tm4(tn, stages, spec);
+  }
+  if (tm == 1) return igf32_pick_mf16_tm1(tn, stages, spec);
+  if (tm == 2) return igf32_pick_mf16_tm2(tn, stages, spec);
+  return igf32_pick_mf16_tm4(tn, stages, spec);
+}
+
+int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
+                     const void* w, void* y, float* ws, void* stream) {
+  using namespace f32g_knob;
+  const ct_op& o = x.op;
+  IgF32Args a;
+  a.N = o.n; a.C = o.c; a.H = o.h; a.W = o.w; a.K = o.k; a.R = o.r; a.S = o.s;
+  a.sh = o.stride_h; a.sw = o.stride_w; a.ph = o.pad_h; a.pw = o.pad_w; a.dh = o.dil_h; a.dw = o.dil_w;
+  a.OH = (int)x.oh; a.OW = (int)x.ow; a.OHW = a.OH * a.OW;
+  a.npix = (int)x.npix; a.kred = (int)x.kred;
+  a.wm = s.knob[WM]; a.wn = s.knob[WN]; a.wsp = s.knob[WS]; a.kc = s.knob[KC];
+  a.bm = g.bm; a.bn = g.bn; a.threads = g.threads;
+  a.cps = g.chunks_per_split; a.chunks = g.chunks;
+  a.a_loads = g.a_loads; a.b_loads = g.b_loads;
+  a.rows_a = g.threads / a.kc; a.rows_b = g.threads / a.bn;
+  a.ny = x.ny;
+  IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);
+  dim3 grid((unsigned)g.tiles_w, (unsigned)g.tiles_k, (unsigned)g.split);
+  float* out = g.split > 1 ? ws : (float*)y;
+  hipLaunchKernelGGL(fn, grid, dim3(g.threads), g.lds_bytes, (hipStream_t)stream, (const float*)xin,
+                     (const float*)w, out, a);
+  if (hipGetLastError() != hipSuccess) return -1;
+  if (g.split > 1) return launch_split_reduce(ws, (float*)y, x.ny, g.split, stream);
+  return 0;
+}
+
+}  // namespace ct

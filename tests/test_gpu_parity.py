@@ -1,0 +1,102 @@
+"""GPU parity of every kernel family against the fp64 oracle, through the C ABI.
+
+Shapes are small enough for the oracle to finish in seconds but span several
+tiles with ragged tails (H, W, K and C not multiples of the tile sizes, C = 3,
+stride 2, 7x7 filters). Each case runs a seeded sample of schedules from the
+op's valid candidate space.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2008_03602_amd import _lib as L, workloads as W
+from gpu_util import check_close, device_ready, make_inputs, note, reference, sched_str, to_device
+
+pytestmark = pytest.mark.gpu
+
+F32_OPS = [
+    W.conv("odd3x3", 1, 5, 13, 11, 3, 1),
+    W.conv("odd3x3s2", 2, 6, 15, 9, 3, 2),
+    W.conv("stem7x7", 1, 3, 29, 10, 7, 2, 3),
+    W.conv("pw_odd", 2, 19, 9, 21, 1, 1, 0),
+    W.conv("pw_s2", 1, 24, 14, 40, 1, 2, 0),
+    W.Op("rect5x3", 1, 7, 12, 17, 12, 5, 3, 1, 2, 2, 1, 1, 1, 1, 0, 0),
+    W.Op("dilated", 1, 4, 11, 11, 6, 3, 3, 1, 1, 2, 2, 2, 2, 1, 0, 0),
+]
+DW_OPS = [
+    W.conv("dw_odd", 2, 13, 15, 13, 3, 1, 1, groups=13),
+    W.conv("dw_s2", 3, 24, 17, 24, 3, 2, 1, groups=24),
+    W.Op("dw5x5", 1, 8, 10, 10, 8, 5, 5, 1, 1, 2, 2, 1, 1, 8, 0, 0),
+]
+BF_OPS = [
+    W.conv("pwbf_odd", 2, 24, 9, 40, 1, 1, 0, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC),
+    W.conv("pwbf_c96", 1, 96, 11, 24, 1, 1, 0, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC),
+    W.conv("pwbf_s2", 1, 40, 13, 72, 1, 2, 0, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC),
+]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    device_ready()
+    yield
+
+
+def _run_sample(op, n_sched, seed, dist="uniform", int_range=2, exact=False):
+    x, w = make_inputs(op, dist, seed=seed, int_range=int_range)
+    ref, a = reference(op, x, w)
+    xd, wd, yd = to_device(op, x, w)
+    scheds = L.ct_sample(op, seed, 99, 0, n_sched)
+    assert len(scheds) > 0
+    fams = set()
+    for s in scheds:
+        tag = "%s %s" % (op.name, sched_str(s))
+        note(tag)
+        yd.fill_(float("nan"))
+        L.conv2d_run(op, s, xd, wd, yd)
+        y = yd.cpu().numpy()
+        split = L.ct_launch_shape(op, s)["kernels"]
+        if exact:
+            assert np.array_equal(y.astype(np.float64), ref), tag + ": not bit-exact on integer inputs"
+        else:
+            check_close(op, y, ref, a, tag, split=4 if split > 1 else 1)
+        fams.add(s.family)
+    return fams
+
+
+@pytest.mark.parametrize("op", F32_OPS, ids=lambda o: o.name)
+def test_fp32_families_match_oracle(op):
+    fams = _run_sample(op, 24, seed=11)
+    assert fams <= {W.FAM_DIRECT_F32, W.FAM_IGEMM_F32}
+
+
+@pytest.mark.parametrize("op", DW_OPS, ids=lambda o: o.name)
+def test_depthwise_matches_oracle(op):
+    _run_sample(op, 24, seed=12)
+
+
+@pytest.mark.parametrize("op", BF_OPS, ids=lambda o: o.name)
+def test_bf16_pointwise_matches_oracle(op):
+    _run_sample(op, 24, seed=13)
+
+
+@pytest.mark.parametrize("op", [F32_OPS[0], F32_OPS[3], DW_OPS[0]], ids=lambda o: o.name)
+def test_integer_inputs_bit_exact_fp32(op):
+    _run_sample(op, 16, seed=21, dist="int", int_range=2, exact=True)
+
+
+@pytest.mark.parametrize("op", [BF_OPS[0], BF_OPS[1]], ids=lambda o: o.name)
+def test_integer_inputs_bit_exact_bf16(op):
+    _run_sample(op, 16, seed=22, dist="int", int_range=8, exact=True)
+
+
+def test_every_family_covered_on_config1_shape():
+    op = W.config(1).ops[0]
+    x, w = make_inputs(op, "uniform", seed=0, config_id=1)
+    ref, a = reference(op, x, w)
+    xd, wd, yd = to_device(op, x, w)
+    scheds = L.ct_sample(op, 0, 1, 0, 64)
+    for s in scheds:
+        note("config1 " + sched_str(s))
+        yd.fill_(float("nan"))
+        L.conv2d_run(op, s, xd, wd, yd)
+        check_close(op, yd.cpu().numpy(), ref, a, "config1 " + sched_str(s), split=4)
