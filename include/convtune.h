@@ -158,6 +158,11 @@ int ct_validate(const ct_op *op, const ct_schedule *s);
 int ct_launch_shape(const ct_op *op, const ct_schedule *s, int32_t *lds_bytes,
                     int32_t *threads, int64_t *blocks, int32_t *kernels);
 
+/* Name of the kernel template instance a schedule launches on op (its main
+ * kernel, as a profiler lists it, e.g. "igemm_f32_kernel<32, 1, 1, 2, 3>"),
+ * NUL-terminated in buf. For reports and for matching profiler traces. */
+int ct_kernel_name(const ct_op *op, const ct_schedule *s, char *buf, int cap);
+
 /* ---- candidate generation (section 2.1 stage 1: with no history, pick
  *      random candidates from the search space) ---- */
 

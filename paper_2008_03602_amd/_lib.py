@@ -79,6 +79,7 @@ _SIGS = {
     "ct_grid_encode": (c_i32, [P(ct_schedule), P(c_i64)]),
     "ct_validate": (c_i32, [P(ct_op), P(ct_schedule)]),
     "ct_launch_shape": (c_i32, [P(ct_op), P(ct_schedule), P(c_i32), P(c_i32), P(c_i64), P(c_i32)]),
+    "ct_kernel_name": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_char_p, c_i32]),
     "ct_valid_space": (c_i32, [P(ct_op), P(ct_schedule), c_i64, P(c_i64)]),
     "ct_sample": (c_i32, [P(ct_op), c_u64, c_i32, c_i32, c_i32, P(ct_schedule), P(c_i32)]),
     "conv2d_run": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -248,6 +249,13 @@ def ct_launch_shape(op, s: ct_schedule):
     _check(lib().ct_launch_shape(ctypes.byref(o), ctypes.byref(s), ctypes.byref(lds), ctypes.byref(th),
                                  ctypes.byref(blocks), ctypes.byref(ker)))
     return {"lds_bytes": lds.value, "threads": th.value, "blocks": blocks.value, "kernels": ker.value}
+
+
+def ct_kernel_name(op, s: ct_schedule) -> str:
+    o = make_op(op)
+    buf = ctypes.create_string_buffer(256)
+    _check(lib().ct_kernel_name(ctypes.byref(o), ctypes.byref(s), buf, 256))
+    return buf.value.decode()
 
 
 def ct_valid_space(op) -> ctypes.Array:

@@ -11,7 +11,7 @@
 
 namespace ct {
 
-constexpr int kMaxLdsBytes = 64 * 1024;   // per-block LDS budget of every schedule
+constexpr int kMaxLdsBytes = 160 * 1024;  // per-block LDS budget (the gfx950 workgroup maximum)
 constexpr int kMaxThreads = 1024;
 constexpr int kMinThreads = 32;
 constexpr int kMaxLoadsPerThread = 8;     // register staging bound of the GEMM loaders
@@ -53,7 +53,7 @@ bool family_applies(int family, const OpX& x);
 namespace direct_knob { enum { TOH, TOW, TK, MK, MW, LDS, CT, SPLIT, UNR, COUNT }; }
 namespace dw_knob { enum { TC, TOH, TOW, VEC, RPT, LDS, NB, ORDER, COUNT }; }
 namespace bf16_knob { enum { MF, TM, TN, WM, WN, KC, LDS, SPLIT, SWZ, COUNT }; }
-namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, KC, STAGES, SPLIT, COUNT }; }
+namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, TPW, CPC, STAGES, SPLIT, COUNT }; }
 
 // Filter/stride specialisation chosen from the op (not a knob).
 enum Spec { SPEC_GENERIC = 0, SPEC_1X1_S1 = 1, SPEC_1X1_S2 = 2, SPEC_3X3_S1 = 3, SPEC_3X3_S2 = 4 };
@@ -75,6 +75,8 @@ struct Geom {
   int chunks;         // reduction chunks in total
   int chunks_per_split;
   int a_loads, b_loads;  // per-thread staged loads per chunk (GEMM families)
+  int kc, kcp;           // reduction rows per chunk, and padded to whole k-steps
+  int cpcp, lda, tph, tpw;  // fp32 MFMA family: padded channels per chunk, filter row pitch, pixel rectangle
 };
 
 // Validates s on x and fills g. Returns CT_OK or CT_S_INVALID (reason in why).

@@ -13,6 +13,7 @@
 #include <hip/hip_runtime.h>
 
 #include "ct_internal.h"
+#include "k_util.h"
 
 namespace ct {
 
@@ -64,7 +65,7 @@ depthwise_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, f
   float wv[RC ? RC * RC : 1];
   if constexpr (RC != 0) {
 #pragma unroll
-    for (int i = 0; i < RC * RC; ++i) wv[i] = live ? w[(int64_t)c * RC * RC + i] : 0.f;
+    for (int i = 0; i < RC * RC; ++i) wv[i] = load_or_zero(w, (int64_t)c * RC * RC + i, live);
   }
   float acc[RPT][VEC];
 #pragma unroll
@@ -77,16 +78,23 @@ depthwise_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, f
     extern __shared__ float smem[];
     const int plane = a.ih_t * a.iw_t;
     const int total = a.nb * a.tc * plane;
-    for (int e = threadIdx.x; e < total; e += a.threads) {
-      const int p = e / plane;  // (image, channel) pair within the block
-      const int rem = e - p * plane;
-      const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
-      const int pn = n0 + p / a.tc, pc = c0 + p % a.tc;
-      const int gh = ih_org + hh, gw = iw_org + ww;
-      float v = 0.f;
-      if (pn < a.N && pc < C && gh >= 0 && gh < H && gw >= 0 && gw < W)
-        v = x[(((int64_t)pn * C + pc) * H + gh) * W + gw];
-      smem[e] = v;
+    // four branch-free loads per thread, then four LDS stores
+    for (int e0 = threadIdx.x; e0 < total; e0 += 4 * a.threads) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + u * a.threads;
+        const int p = e / plane;  // (image, channel) pair within the block
+        const int rem = e - p * plane;
+        const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
+        const int pn = n0 + p / a.tc, pc = c0 + p % a.tc;
+        const int gh = ih_org + hh, gw = iw_org + ww;
+        const bool ok = e < total && pn < a.N && pc < C && gh >= 0 && gh < H && gw >= 0 && gw < W;
+        v[u] = load_or_zero(x, (((int64_t)pn * C + pc) * H + gh) * W + gw, ok);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (e0 + u * a.threads < total) smem[e0 + u * a.threads] = v[u];
     }
     __syncthreads();
     const float* xs = smem + (ni * a.tc + ci) * plane;
@@ -121,7 +129,7 @@ depthwise_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, f
 #pragma unroll
           for (int v = 0; v < VEC; ++v) {
             const int gw = (ow0 + colg + v * a.cols) * sw - pw + s * dw;
-            const float xv = (hok && gw >= 0 && gw < W) ? xc[(int64_t)gh * W + gw] : 0.f;
+            const float xv = load_or_zero(xc, (int64_t)gh * W + gw, hok && gw >= 0 && gw < W);
             acc[u][v] = fmaf(wt, xv, acc[u][v]);
           }
         }

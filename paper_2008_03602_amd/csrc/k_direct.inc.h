@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include "ct_internal.h"
+#include "k_util.h"
 
 namespace ct {
 
@@ -76,24 +77,40 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
       float* wsm = smem + a.ct * a.ih_t * a.iw_t;
       const int plane = a.ih_t * a.iw_t;
       const int xt = a.ct * plane;
-      for (int e = t; e < xt; e += a.threads) {
-        const int c = e / plane;
-        const int rem = e - c * plane;
-        const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
-        const int gh = ih_org + hh, gw = iw_org + ww;
-        float v = 0.f;
-        if (c < nc && gh >= 0 && gh < H && gw >= 0 && gw < W) v = xn[((int64_t)(cc + c) * H + gh) * W + gw];
-        xs[e] = v;
+      // Stage the halo tile and the filter chunk four elements per thread at a
+      // time: four branch-free loads, then four LDS stores.
+      for (int e0 = t; e0 < xt; e0 += 4 * a.threads) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + u * a.threads;
+          const int c = e / plane;
+          const int rem = e - c * plane;
+          const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
+          const int gh = ih_org + hh, gw = iw_org + ww;
+          const bool ok = e < xt && c < nc && gh >= 0 && gh < H && gw >= 0 && gw < W;
+          v[u] = load_or_zero(xn, ((int64_t)(cc + c) * H + gh) * W + gw, ok);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (e0 + u * a.threads < xt) xs[e0 + u * a.threads] = v[u];
       }
       const int crs = a.ct * RS;
       const int wt = a.tk * crs;
-      for (int e = t; e < wt; e += a.threads) {
-        const int kk = e / crs;
-        const int rem = e - kk * crs;
-        const int c = rem / RS, rs = rem - c * RS;
-        float v = 0.f;
-        if (k0 + kk < K && c < nc) v = w[((int64_t)(k0 + kk) * C + cc + c) * RS + rs];
-        wsm[e] = v;
+      for (int e0 = t; e0 < wt; e0 += 4 * a.threads) {
+        float v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + u * a.threads;
+          const int kk = e / crs;
+          const int rem = e - kk * crs;
+          const int c = rem / RS, rs = rem - c * RS;
+          const bool ok = e < wt && k0 + kk < K && c < nc;
+          v[u] = load_or_zero(w, ((int64_t)(k0 + kk) * C + cc + c) * RS + rs, ok);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (e0 + u * a.threads < wt) wsm[e0 + u * a.threads] = v[u];
       }
       __syncthreads();
 #pragma unroll UNR
@@ -130,12 +147,12 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
             for (int j = 0; j < MW; ++j) {
               const int ow = ow0 + lc + j * a.cols;
               const int gw = ow * sw - pw + s * dw;
-              xv[j] = (hok && gw >= 0 && gw < W) ? xc[(int64_t)gh * W + gw] : 0.f;
+              xv[j] = load_or_zero(xc, (int64_t)gh * W + gw, hok && gw >= 0 && gw < W);
             }
 #pragma unroll
             for (int i = 0; i < MK; ++i) {
               const int k = kbase + i;
-              wv[i] = k < K ? w[((int64_t)k * C + cc + c) * RS + r * S + s] : 0.f;
+              wv[i] = load_or_zero(w, ((int64_t)k * C + cc + c) * RS + r * S + s, k < K);
             }
 #pragma unroll
             for (int i = 0; i < MK; ++i)

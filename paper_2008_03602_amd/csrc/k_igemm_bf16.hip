@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 
 #include "ct_internal.h"
+#include "k_util.h"
 
 namespace ct {
 
@@ -54,7 +55,7 @@ struct MfmaBf16<32> {
   __device__ static int row(int e, int lane) { return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3); }
 };
 
-__host__ __device__ constexpr int bf16_max_threads(int acc_regs) { return acc_regs <= 32 ? 1024 : (acc_regs <= 64 ? 512 : 256); }
+__host__ __device__ constexpr int bf16_max_threads(int acc_regs) { return acc_regs <= 64 ? 512 : 256; }
 constexpr int kBf16MaxSteps = 4;  // k-steps of fragments held in registers (LDS = 0)
 
 __device__ inline int pixel_offset(int m, const IgBf16Args& a) {
@@ -66,10 +67,12 @@ __device__ inline int pixel_offset(int m, const IgBf16Args& a) {
   return ((n * a.H + oh * a.sh) * a.W + ow * a.sw) * a.C;
 }
 
-__device__ inline bf16x8 load8(const unsigned short* p, bool ok) {
-  u32x4 v = {0u, 0u, 0u, 0u};
-  if (ok) v = *(const u32x4*)p;
-  return __builtin_bit_cast(bf16x8, v);
+// 16-byte fragment load, branch-free: an invalid fragment reads the tensor's
+// first 16 bytes and is replaced by zeros.
+__device__ inline bf16x8 load8(const unsigned short* base, int64_t off, bool ok) {
+  const u32x4 v = *(const u32x4*)(base + (ok ? off : 0));
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  return __builtin_bit_cast(bf16x8, ok ? v : z);
 }
 
 template <int MF, int TM, int TN, bool LDS>
@@ -90,7 +93,7 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
   const int tmi = b / a.tiles_n, tni = b - tmi * a.tiles_n;
   const int m0 = tmi * a.bm, n0 = tni * a.bn, sp = blockIdx.y;
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63, wave = wave_id();
   const int wmi = wave / a.wn, wni = wave - wmi * a.wn;
   const int m_off = wmi * TM * MF, n_off = wni * TN * MF;
   const int lrow = lane % MF, kq = (lane / MF) * 8;  // fragment row and k offset of this lane
@@ -131,9 +134,9 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
         const int k = kr0 + st * KSTEP + kq;
         const bool kok = st < steps && k < kr_end;
 #pragma unroll
-        for (int i = 0; i < TM; ++i) fa[st][i] = load8(x + aoff[i] + k, kok && aok[i]);
+        for (int i = 0; i < TM; ++i) fa[st][i] = load8(x, (int64_t)aoff[i] + k, kok && aok[i]);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[st][j] = load8(w + boff[j] + k, kok && bok[j]);
+        for (int j = 0; j < TN; ++j) fb[st][j] = load8(w, (int64_t)boff[j] + k, kok && bok[j]);
       }
 #pragma unroll
       for (int st = 0; st < kBf16MaxSteps; ++st) {
@@ -163,25 +166,35 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
     for (int ch = ch_begin; ch < ch_end; ++ch) {
       const int k = ch * a.kc + vcol * 8;
       const bool kok = k < kr_end;
+      // loads are issued unconditionally (invalid ones read offset 0) and the
+      // zero-select happens at the LDS store, so all loads are in flight at once
       u32x4 ra[kMaxLoadsPerThread], rb[kMaxLoadsPerThread];
+      unsigned oka = 0, okb = 0;
 #pragma unroll
       for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-        ra[i] = u32x4{0u, 0u, 0u, 0u};
-        if (kok && aok[i]) ra[i] = *(const u32x4*)(x + aoff[i] + k);
+        if (i < a.a_loads) {
+          const bool ok = kok && aok[i];
+          ra[i] = *(const u32x4*)(x + (ok ? (int64_t)aoff[i] + k : 0));
+          oka |= (unsigned)ok << i;
+        }
       }
 #pragma unroll
       for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-        const int rr = row0 + i * rstep;
-        const int n = n0 + rr;
-        rb[i] = u32x4{0u, 0u, 0u, 0u};
-        if (i < a.b_loads && rr < a.bn && n < a.K && kok) rb[i] = *(const u32x4*)(w + (int64_t)n * a.C + k);
+        if (i < a.b_loads) {
+          const int rr = row0 + i * rstep;
+          const int n = n0 + rr;
+          const bool ok = rr < a.bn && n < a.K && kok;
+          rb[i] = *(const u32x4*)(w + (ok ? (int64_t)n * a.C + k : 0));
+          okb |= (unsigned)ok << i;
+        }
       }
       __syncthreads();
+      const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
       for (int i = 0; i < kMaxLoadsPerThread; ++i) {
         const int rr = row0 + i * rstep;
-        if (i < a.a_loads && rr < a.bm) *(u32x4*)(As + rr * pitch + vcol * 8) = ra[i];
-        if (i < a.b_loads && rr < a.bn) *(u32x4*)(Bs + rr * pitch + vcol * 8) = rb[i];
+        if (i < a.a_loads && rr < a.bm) *(u32x4*)(As + rr * pitch + vcol * 8) = (oka >> i & 1u) ? ra[i] : z;
+        if (i < a.b_loads && rr < a.bn) *(u32x4*)(Bs + rr * pitch + vcol * 8) = (okb >> i & 1u) ? rb[i] : z;
       }
       __syncthreads();
       const int steps = a.kc / KSTEP;

@@ -29,16 +29,16 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   IgF32Args a;
   a.N = o.n; a.C = o.c; a.H = o.h; a.W = o.w; a.K = o.k; a.R = o.r; a.S = o.s;
   a.sh = o.stride_h; a.sw = o.stride_w; a.ph = o.pad_h; a.pw = o.pad_w; a.dh = o.dil_h; a.dw = o.dil_w;
-  a.OH = (int)x.oh; a.OW = (int)x.ow; a.OHW = a.OH * a.OW;
-  a.npix = (int)x.npix; a.kred = (int)x.kred;
-  a.wm = s.knob[WM]; a.wn = s.knob[WN]; a.wsp = s.knob[WS]; a.kc = s.knob[KC];
+  a.OH = (int)x.oh; a.OW = (int)x.ow; a.kred = (int)x.kred;
+  a.wm = s.knob[WM]; a.wn = s.knob[WN]; a.wsp = s.knob[WS]; a.cpc = s.knob[CPC]; a.cpcp = g.cpcp;
+  a.tpw = g.tpw; a.tph = g.tph; a.tiles_w = (int)g.tiles_w; a.tiles_h = (int)g.tiles_h;
+  a.ht = g.ih_t; a.wt = g.iw_t; a.lda = g.lda;
   a.bm = g.bm; a.bn = g.bn; a.threads = g.threads;
   a.cps = g.chunks_per_split; a.chunks = g.chunks;
-  a.a_loads = g.a_loads; a.b_loads = g.b_loads;
-  a.rows_a = g.threads / a.kc; a.rows_b = g.threads / a.bn;
+  a.n_halo = g.a_loads; a.n_filt = g.b_loads;
   a.ny = x.ny;
   IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);
-  dim3 grid((unsigned)g.tiles_w, (unsigned)g.tiles_k, (unsigned)g.split);
+  dim3 grid((unsigned)(o.n * g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.split);
   float* out = g.split > 1 ? ws : (float*)y;
   hipLaunchKernelGGL(fn, grid, dim3(g.threads), g.lds_bytes, (hipStream_t)stream, (const float*)xin,
                      (const float*)w, out, a);

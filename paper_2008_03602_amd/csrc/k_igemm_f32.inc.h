@@ -2,44 +2,58 @@
 // cores (v_mfma_f32_32x32x2_f32 / v_mfma_f32_16x16x4_f32), NCHW x,
 // K x C x R x S w, NCHW y.
 //
-// GEMM view: rows = output channels (K), columns = output pixels
-// (N*OH*OW, flattened), reduction = C*R*S in the filter's memory order, so
-// the A operand (filter) is a plain row-major matrix and the B operand is the
-// im2col gather of x, formed on the fly and never stored in HBM.
+// GEMM view: rows = output channels, columns = output pixels, reduction =
+// (filter tap, input channel). A block owns a BM x BN tile: BM = WM*TM*MF
+// output channels by BN = WN*TN*MF output pixels, the pixels forming a
+// TPH x TPW rectangle of one image (TPW = the TPW knob, TPH = BN / TPW).
 //
-// A block owns a BM x BN tile (BM = WM*TM*MF channels, BN = WN*TN*MF pixels)
-// and WS reduction groups of WM x WN waves. Each reduction chunk of KC is
-// staged in LDS (A as [BM][KC+1], B as [KC][BN]); reduction group g does the
-// g-th share of the chunk's MFMA k-steps, and the groups' partial tiles are
-// added in group order through LDS at the end. STAGES = 2 double-buffers the
-// LDS tile and keeps the next chunk's global loads in flight during the
-// MFMAs. SPLIT > 1 spreads contiguous chunk ranges over grid.z and adds the
-// partial outputs in split order in a second kernel.
+// Staging. The reduction advances one chunk of CPC input channels at a time
+// (padded to CPCP, a whole number of MFMA k-groups per reduction group). A
+// chunk stages in LDS
+//   * the input halo of the pixel rectangle, Xs[CPCP][HT][WT], loaded once:
+//     every filter tap reads its operand from this tile, so a 3x3 filter
+//     costs one global load per input element instead of nine;
+//   * the filter slice As[BM][R*S][CPCP] (row pitch LDA), tap-major so that
+//     consecutive MFMA k-steps are consecutive channels of one tap.
+// Global reads are raw buffer loads: the descriptor base advances one chunk
+// per iteration (scalar work); per-lane byte offsets are fixed for the whole
+// kernel, and an element that is padding, overhang or a padded channel gets
+// an offset beyond the buffer, which reads as 0. The staging plan is built
+// with carry counters (no per-element divisions).
 //
-// All global loads are bounds-checked (zero fill), so any tile overhang and
-// any ragged reduction tail are safe.
+// MFMA k mapping. k lane-group g (= lane / MF) takes channels i*KSTEP + g,
+// so for a fixed tap a step advances every operand address by a constant:
+// A by KSTEP, B by KSTEP channel planes of the halo. WS reduction groups
+// split the k-steps of each tap; their partial tiles are added in group order
+// through LDS. STAGES = 2 double-buffers the LDS chunk and keeps the next
+// chunk's loads in flight during the MFMAs. SPLIT > 1 spreads contiguous chunk
+// ranges over grid.z; a second kernel adds the partials in split order.
 #pragma once
 #include <hip/hip_runtime.h>
 
 #include "ct_internal.h"
+#include "k_util.h"
 
 namespace ct {
 
+constexpr int kF32Slots = 16;  // staged elements per thread per chunk: halo + filter (max)
+
 struct IgF32Args {
   int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
-  int OH, OW, OHW;
-  int npix, kred;
-  int wm, wn, wsp, kc;
+  int OH, OW, kred;
+  int wm, wn, wsp, cpc, cpcp;
+  int tpw, tph, tiles_w, tiles_h;
+  int ht, wt, lda;
   int bm, bn, threads;
   int cps, chunks;
-  int a_loads, b_loads, rows_a, rows_b;
+  int n_halo, n_filt;  // staged halo / filter elements per thread per chunk
   int64_t ny;
 };
 
 __host__ __device__ constexpr int ig_spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
 __host__ __device__ constexpr int ig_spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
 // Threads per block that leave room for the accumulator tile in registers.
-__host__ __device__ constexpr int mfma_max_threads(int acc_regs) { return acc_regs <= 32 ? 1024 : (acc_regs <= 64 ? 512 : 256); }
+__host__ __device__ constexpr int mfma_max_threads(int acc_regs) { return acc_regs <= 64 ? 512 : 256; }
 
 template <int MF>
 struct MfmaF32;
@@ -59,6 +73,15 @@ struct MfmaF32<16> {
   __device__ static int row(int e, int lane) { return 4 * (lane >> 4) + e; }
 };
 
+constexpr int kOob = 0x7FFFFFF0;  // byte offset beyond every buffer: reads as 0
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t r, int off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
 template <int MF, int TM, int TN, int STAGES, int SPEC>
 __global__ void __launch_bounds__(mfma_max_threads(TM * TN * MfmaF32<MF>::ACC))
 igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ out,
@@ -72,81 +95,121 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int dh = SPEC ? 1 : a.dh, dw = SPEC ? 1 : a.dw;
   const int ph = SPEC ? RC / 2 : a.ph, pw = SPEC ? RC / 2 : a.pw;
   const int RS = R * S;
+  const int HW = a.H * a.W;
 
   extern __shared__ float smem[];
-  const int kc = a.kc, bm = a.bm, bn = a.bn;
-  const int a_pitch = kc + 1;
-  const int stage_floats = bm * a_pitch + kc * bn;
+  const int cpcp = a.cpcp, bm = a.bm, ht = a.ht, wt = a.wt, lda = a.lda;
+  const int plane = ht * wt;
+  const int xs_floats = cpcp * plane;
+  const int stage_floats = xs_floats + bm * lda;
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63, wave = wave_id();
   const int wpg = a.wm * a.wn;
   const int wg = wave / wpg, wi = wave - wg * wpg;
   const int wmi = wi / a.wn, wni = wi - wmi * a.wn;
   const int m_off = wmi * TM * MF, n_off = wni * TN * MF;
-  const int p0 = blockIdx.x * bn, k0 = blockIdx.y * bm, sp = blockIdx.z;
 
-  // loader coordinates: A = filter rows of this block, B = im2col columns
-  const int kr_a = t % kc, row_a0 = t / kc;
-  const int pp = t % bn, krow_b0 = t / bn;
-  const int p = p0 + pp;
-  const bool pvalid = p < a.npix;
-  int ih0 = 0, iw0 = 0, nimg = 0;
-  if (pvalid) {
-    nimg = p / a.OHW;
-    const int rem = p - nimg * a.OHW;
-    const int oh = rem / a.OW, ow = rem - oh * a.OW;
-    ih0 = oh * sh - ph;
-    iw0 = ow * sw - pw;
+  // block -> (image, pixel rectangle), output-channel tile, split
+  const int tiles_hw = a.tiles_h * a.tiles_w;
+  const int nimg = blockIdx.x / tiles_hw;
+  const int trem = blockIdx.x - nimg * tiles_hw;
+  const int th = trem / a.tiles_w, tw = trem - th * a.tiles_w;
+  const int oh0 = th * a.tph, ow0 = tw * a.tpw;
+  const int ih0 = oh0 * sh - ph, iw0 = ow0 * sw - pw;
+  const int k0 = blockIdx.y * bm, sp = blockIdx.z;
+
+  // ---- staging plan, fixed for the whole reduction (carry counters) ----
+  // Each thread stages kF32Slots elements per chunk: slots [0, n_halo) are
+  // halo elements, the next n_filt are filter elements, the rest are unused.
+  // Every slot issues its load (an unused or padding slot reads out of range,
+  // i.e. 0) and stores to LDS (an unused slot into a per-lane dummy word), so
+  // the staging code has no branches and all loads are in flight at once.
+  const int dummy = STAGES * stage_floats + lane;
+  int s_off[kF32Slots], s_lds[kF32Slots];
+  {
+    // halo element e = t + i*threads of Xs[cpcp][ht][wt] -> (c, hh, ww)
+    const int T = a.threads;
+    int c = t / plane, rem = t - c * plane;
+    int hh = rem / wt, ww = rem - hh * wt;
+    const int dc = T / plane, drem = T - dc * plane;
+    const int dhh = drem / wt, dww = drem - dhh * wt;
+#pragma unroll
+    for (int i = 0; i < kF32Slots; ++i) {
+      if (i < a.n_halo) {
+        const int gh = ih0 + hh, gw = iw0 + ww;
+        const int e = t + i * T;
+        const bool ok = c < a.cpc && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
+        s_off[i] = ok ? ((nimg * a.C + c) * HW + gh * a.W + gw) * 4 : kOob;
+        s_lds[i] = e < xs_floats ? e : -1;
+        ww += dww;
+        if (ww >= wt) { ww -= wt; ++hh; }
+        hh += dhh;
+        if (hh >= ht) { hh -= ht; ++c; }
+        c += dc;
+      }
+    }
   }
-  const float* xn = x + (int64_t)nimg * a.C * a.H * a.W;
+  {
+    // filter element e = t + j*threads of the chunk's BM x CPCP x RS slice, in
+    // global order (m, c, tap); LDS position m*lda + tap*cpcp + c
+    const int T = a.threads, per_m = cpcp * RS;
+    int m = t / per_m, rem = t - m * per_m;
+    int c = rem / RS, tap = rem - c * RS;
+    const int dm = T / per_m, drem = T - dm * per_m;
+    const int dcc = drem / RS, dtap = drem - dcc * RS;
+#pragma unroll
+    for (int i = 0; i < kF32Slots; ++i) {
+      const int j = i - a.n_halo;
+      if (j >= 0 && j < a.n_filt) {
+        const bool in_tile = m < bm;
+        const bool ok = in_tile && k0 + m < a.K && c < a.cpc;
+        s_off[i] = ok ? ((k0 + m) * a.kred + c * RS + tap) * 4 : kOob;
+        s_lds[i] = in_tile ? xs_floats + m * lda + tap * cpcp + c : -1;
+        tap += dtap;
+        if (tap >= RS) { tap -= RS; ++c; }
+        c += dcc;
+        if (c >= cpcp) { c -= cpcp; ++m; }
+        m += dm;
+      } else if (j >= a.n_filt) {
+        s_off[i] = kOob;
+        s_lds[i] = -1;
+      }
+    }
+  }
+  // A partial last chunk (C not a multiple of CPC) masks the channels it lacks;
+  // this runs once, before that chunk's loads are issued.
+  auto mask_missing_channels = [&](int cl) {
+#pragma unroll
+    for (int i = 0; i < kF32Slots; ++i) {
+      int c;
+      if (i < a.n_halo) {
+        c = (t + i * a.threads) / plane;
+      } else {
+        const int e = t + (i - a.n_halo) * a.threads;
+        c = (e % (cpcp * RS)) / RS;
+      }
+      if (c >= cl) s_off[i] = kOob;
+    }
+  };
 
   const int ch_begin = sp * a.cps;
   const int ch_end = min(a.chunks, ch_begin + a.cps);
-  const int kr_end = min(a.kred, ch_end * kc);
+  const int64_t xbytes = (int64_t)a.N * a.C * HW * 4, wbytes = (int64_t)a.K * a.kred * 4;
 
-  float ra[kMaxLoadsPerThread], rb[kMaxLoadsPerThread];
+  float rv[kF32Slots];
   auto load_chunk = [&](int ch) {
-    const int kr0 = ch * kc;
+    const int c0 = ch * a.cpc;
+    if (c0 + a.cpc > a.C) mask_missing_channels(a.C - c0);
+    // descriptors start at the chunk's first channel
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)c0 * HW, xbytes - (int64_t)c0 * HW * 4);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)c0 * RS, wbytes - (int64_t)c0 * RS * 4);
 #pragma unroll
-    for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-      if (i < a.a_loads) {
-        const int row = row_a0 + i * a.rows_a;
-        const int kr = kr0 + kr_a;
-        float v = 0.f;
-        if (row < bm && k0 + row < a.K && kr < kr_end) v = w[(int64_t)(k0 + row) * a.kred + kr];
-        ra[i] = v;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-      if (i < a.b_loads) {
-        const int krow = krow_b0 + i * a.rows_b;
-        const int kr = kr0 + krow;
-        float v = 0.f;
-        if (pvalid && krow < kc && kr < kr_end) {
-          const int c = kr / RS;
-          const int rs = kr - c * RS;
-          const int r = rs / S, s = rs - r * S;
-          const int ih = ih0 + r * dh, iw = iw0 + s * dw;
-          if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W) v = xn[((int64_t)c * a.H + ih) * a.W + iw];
-        }
-        rb[i] = v;
-      }
-    }
+    for (int i = 0; i < kF32Slots; ++i) rv[i] = bload(i < a.n_halo ? rx : rw, s_off[i]);
   };
   auto store_chunk = [&](int stage) {
-    float* As = smem + stage * stage_floats;
-    float* Bs = As + bm * a_pitch;
+    const int base = stage * stage_floats;
 #pragma unroll
-    for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-      const int row = row_a0 + i * a.rows_a;
-      if (i < a.a_loads && row < bm) As[row * a_pitch + kr_a] = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxLoadsPerThread; ++i) {
-      const int krow = krow_b0 + i * a.rows_b;
-      if (i < a.b_loads && krow < kc) Bs[krow * bn + pp] = rb[i];
-    }
+    for (int i = 0; i < kF32Slots; ++i) smem[s_lds[i] >= 0 ? base + s_lds[i] : dummy] = rv[i];
   };
 
   V acc[TM][TN];
@@ -157,24 +220,56 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 #pragma unroll
       for (int e = 0; e < ACC; ++e) acc[i][j][e] = 0.f;
 
-  const int spg = (kc / KSTEP) / a.wsp;  // k-steps per reduction group
-  const int lrow = lane % MF, kl_lane = lane / MF;
+  // this lane's operand bases: A row (output channel), B pixel in the halo
+  const int lrow = lane % MF, kg = lane / MF;
+  int a_base[TM], b_base[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) a_base[i] = (m_off + i * MF + lrow) * lda + kg;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int q = n_off + j * MF + lrow;
+    const int pr = q / a.tpw, pc = q - pr * a.tpw;
+    b_base[j] = kg * plane + (pr * sh) * wt + pc * sw;
+  }
+  const int n_i = cpcp / KSTEP / a.wsp;  // k-steps per tap for this reduction group
+  const int i_begin = wg * n_i;
   auto compute = [&](int stage) {
-    const float* As = smem + stage * stage_floats;
-    const float* Bs = As + bm * a_pitch;
-    const float* ap = As + (m_off + lrow) * a_pitch + kl_lane;
-    const float* bp = Bs + kl_lane * bn + n_off + lrow;
-    for (int st = wg * spg; st < (wg + 1) * spg; ++st) {
-      const int kb = st * KSTEP;
-      float fa[TM], fb[TN];
+    const float* Xs = smem + stage * stage_floats;
+    const float* As = Xs + xs_floats;
+    for (int r = 0; r < R; ++r) {
+      for (int s = 0; s < S; ++s) {
+        const int tap = r * S + s;
+        const float* ap = As + tap * cpcp + i_begin * KSTEP;
+        const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * KSTEP * plane;
+        int ii = 0;
+        for (; ii + 2 <= n_i; ii += 2) {
+          float fa[2][TM], fb[2][TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = ap[i * MF * a_pitch + kb];
+          for (int u = 0; u < 2; ++u) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = bp[kb * bn + j * MF];
+            for (int i = 0; i < TM; ++i) fa[u][i] = ap[a_base[i] + (ii + u) * KSTEP];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+            for (int j = 0; j < TN; ++j) fb[u][j] = bp[b_base[j] + (ii + u) * KSTEP * plane];
+          }
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[i], fb[j], acc[i][j]);
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+              for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[u][i], fb[u][j], acc[i][j]);
+        }
+        if (ii < n_i) {
+          float fa[TM], fb[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * KSTEP];
+#pragma unroll
+          for (int j = 0; j < TN; ++j) fb[j] = bp[b_base[j] + ii * KSTEP * plane];
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[i], fb[j], acc[i][j]);
+        }
+      }
     }
   };
 
@@ -231,17 +326,17 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   float* o = out + (int64_t)sp * a.ny;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    const int pq = p0 + n_off + j * MF + lrow;
-    if (pq >= a.npix) continue;
-    const int ni = pq / a.OHW;
-    const int rem = pq - ni * a.OHW;
-    float* op = o + (int64_t)ni * a.K * a.OHW + rem;
+    const int q = n_off + j * MF + lrow;
+    const int pr = q / a.tpw, pc = q - pr * a.tpw;
+    const int oh = oh0 + pr, ow = ow0 + pc;
+    if (oh >= a.OH || ow >= a.OW) continue;
+    float* op = o + ((int64_t)nimg * a.K * a.OH + oh) * a.OW + ow;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int e = 0; e < ACC; ++e) {
         const int k = k0 + m_off + i * MF + M::row(e, lane);
-        if (k < a.K) op[(int64_t)k * a.OHW] = acc[i][j][e];
+        if (k < a.K) op[(int64_t)k * a.OH * a.OW] = acc[i][j][e];
       }
     }
   }

@@ -1,0 +1,21 @@
+// Device helpers shared by the kernel families.
+#pragma once
+#include <hip/hip_runtime.h>
+
+namespace ct {
+
+// Bounds-checked load without a branch: the address is clamped to element 0
+// when `ok` is false and the value is replaced by zero. Keeping loads out of
+// divergent branches lets the compiler issue a whole batch of them before the
+// first wait, instead of waiting for each one in turn.
+template <typename T>
+__device__ __forceinline__ T load_or_zero(const T* __restrict__ p, int64_t idx, bool ok) {
+  const T v = p[ok ? idx : 0];
+  return ok ? v : T{};
+}
+
+// The wave index as a scalar value, so loops bounded by per-wave values stay
+// uniform (scalar branches, unrollable) instead of exec-masked.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
+}  // namespace ct

@@ -3,6 +3,7 @@
 // selection and CU-mask construction. No HIP calls in this file.
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -52,7 +53,8 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"wm", 3, {1, 2, 4}},
       {"wn", 3, {1, 2, 4}},
       {"ws", 3, {1, 2, 4}},
-      {"kc", 3, {8, 16, 32}},
+      {"tpw", 4, {8, 16, 32, 64}},
+      {"cpc", 6, {1, 2, 4, 8, 16, 32}},
       {"stages", 2, {1, 2}},
       {"split", 4, {1, 2, 4, 8}}}},
 };
@@ -150,7 +152,7 @@ static int32_t fit_pow2(int64_t extent, int32_t lo, int32_t hi) {
 
 // Block size that leaves room for an MFMA accumulator tile of acc_regs
 // registers per lane (the kernels declare the same bound).
-static int mfma_thread_limit(int acc_regs) { return acc_regs <= 32 ? 1024 : (acc_regs <= 64 ? 512 : 256); }
+static int mfma_thread_limit(int acc_regs) { return acc_regs <= 64 ? 512 : 256; }
 
 static bool knobs_in_table(const FamilyDef& f, const ct_schedule& s) {
   for (int i = 0; i < f.nknobs; ++i) {
@@ -294,41 +296,59 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const FamilyDef& f = *family_def(CT_FAM_IGEMM_F32);
   const ct_op& o = x.op;
   const int mf = s.knob[MF], tm = s.knob[TM], tn = s.knob[TN], wm = s.knob[WM], wn = s.knob[WN];
-  const int wsplit = s.knob[WS], kc = s.knob[KC], stages = s.knob[STAGES], split = s.knob[SPLIT];
+  const int wsplit = s.knob[WS], tpw = s.knob[TPW], cpc = s.knob[CPC], stages = s.knob[STAGES];
+  const int split = s.knob[SPLIT];
   const int bm = wm * tm * mf;  // output channels per block
-  const int bn = wn * tn * mf;  // pixels per block
+  const int bn = wn * tn * mf;  // output pixels per block: a tph x tpw rectangle
   if (bm > fit_pow2(o.k, 16, 512)) REJECT("block rows exceed K");
-  if (bn > fit_pow2(x.npix, 16, 1024)) REJECT("block columns exceed the pixel count");
-  if (kc > fit(f.knobs[KC], x.kred)) REJECT("kc exceeds the reduction length");
+  if (bn % tpw) REJECT("pixel tile is not a whole number of rows");
+  const int tph = bn / tpw;
+  if (tpw > fit_pow2(x.ow, 8, 64)) REJECT("pixel tile wider than the output");
+  if (tph > fit_pow2(x.oh, 1, 1024)) REJECT("pixel tile taller than the output");
+  if (cpc > fit(f.knobs[CPC], x.cg)) REJECT("channels per chunk exceed C");
   const int acc_regs = tm * tn * (mf == 32 ? 16 : 4);
   if (acc_regs > 128) REJECT("accumulator tile too large");
-  const int kstep = mf == 32 ? 2 : 4;
-  if (wsplit > kc / kstep) REJECT("more reduction waves than steps in a chunk");
   const int threads = 64 * wm * wn * wsplit;
   if (threads > mfma_thread_limit(acc_regs)) REJECT("too many threads for the accumulator tile");
-  if (bn > threads) REJECT("block columns exceed the thread count");
-  const int rows_b = threads / bn;  // chunk rows loaded per pass (B)
-  const int rows_a = threads / kc;  // filter rows loaded per pass (A)
-  g->b_loads = (int)cdiv(kc, rows_b);
-  g->a_loads = (int)cdiv(bm, rows_a);
-  if (g->a_loads > kMaxLoadsPerThread || g->b_loads > kMaxLoadsPerThread)
-    REJECT("too many staged loads per thread");
-  const int64_t chunks = cdiv(x.kred, kc);
+  // channels per chunk padded to whole k-steps for every reduction group
+  const int kstep = mf == 32 ? 2 : 4;
+  const int cpcp = (int)cdiv(cpc, kstep * wsplit) * kstep * wsplit;
+  if (cpcp > 2 * cpc && cpc < x.cg) REJECT("chunk padding exceeds the chunk");
+  const int rs = o.r * o.s;
+  const int ht = (tph - 1) * o.stride_h + (o.r - 1) * o.dil_h + 1;
+  const int wt = (tpw - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1;
+  const int lda = rs * cpcp + 1;
+  const int64_t xs = (int64_t)cpcp * ht * wt;
+  g->a_loads = (int)cdiv(xs, threads);                       // halo elements per thread
+  g->b_loads = (int)cdiv((int64_t)bm * cpcp * rs, threads);  // filter elements per thread
+  if (g->a_loads + g->b_loads > 16) REJECT("too many staged loads per thread");
+  if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
+    REJECT("tensor too large for 32-bit buffer offsets");
+  const int64_t chunks = cdiv(x.cg, cpc);
   int64_t cps = 0;
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty reduction range");
-  const int64_t stage_bytes = 4 * ((int64_t)bm * (kc + 1) + (int64_t)kc * bn);
+  const int64_t stage_bytes = 4 * (xs + (int64_t)bm * lda);
   const int64_t red_bytes = wsplit > 1 ? 4 * (int64_t)(wsplit - 1) * bm * bn : 0;
-  const int64_t lbytes = std::max(stages * stage_bytes, red_bytes);
+  // + one word per lane where unused staging slots land
+  const int64_t lbytes = std::max(stages * stage_bytes + 256, red_bytes);
   if (lbytes > kMaxLdsBytes) REJECT("LDS tile too large");
   g->bm = bm;
   g->bn = bn;
+  g->cpcp = cpcp;
+  g->lda = lda;
+  g->tph = tph;
+  g->tpw = tpw;
+  g->ih_t = ht;
+  g->iw_t = wt;
+  g->tiles_h = cdiv(x.oh, tph);
+  g->tiles_w = cdiv(x.ow, tpw);
   g->tiles_k = cdiv(o.k, bm);
-  g->tiles_w = cdiv(x.npix, bn);
   g->tiles_n = split;
   if (g->tiles_k > 65535) REJECT("grid too large");
+  if ((int64_t)o.n * g->tiles_h * g->tiles_w >= ((int64_t)1 << 31)) REJECT("grid too large");
   g->threads = threads;
   g->lds_bytes = (int)lbytes;
-  g->blocks = g->tiles_w * g->tiles_k * split;
+  g->blocks = (int64_t)o.n * g->tiles_h * g->tiles_w * g->tiles_k * split;
   g->split = split;
   g->chunks = (int)chunks;
   g->chunks_per_split = (int)cps;
@@ -462,6 +482,39 @@ int ct_launch_shape(const ct_op* op, const ct_schedule* s, int32_t* lds_bytes, i
   if (threads) *threads = g.threads;
   if (blocks) *blocks = g.blocks;
   if (kernels) *kernels = g.kernels;
+  return CT_OK;
+}
+
+int ct_kernel_name(const ct_op* op, const ct_schedule* s, char* buf, int cap) {
+  if (!op || !s || !buf || cap <= 0) { set_error("ct_kernel_name: bad argument"); return CT_E_ARG; }
+  OpX x;
+  std::string why;
+  if (!derive_op(*op, &x, &why)) { set_error(why); return CT_E_ARG; }
+  Geom g;
+  if (compute_geom(x, *s, &g, &why) != CT_OK) { set_error("invalid schedule: " + why); return CT_E_ARG; }
+  const int* k = s->knob;
+  auto tf = [](int v) { return v ? "true" : "false"; };
+  char tmp[128];
+  switch (s->family) {
+    case CT_FAM_DIRECT_F32:
+      std::snprintf(tmp, sizeof tmp, "direct_f32_kernel<%d, %d, %s, %d, %d>", k[direct_knob::MK],
+                    k[direct_knob::MW], tf(k[direct_knob::LDS]), (int)g.spec, k[direct_knob::UNR]);
+      break;
+    case CT_FAM_DEPTHWISE_F32: {
+      const int spec = g.spec == SPEC_3X3_S1 ? 3 : (g.spec == SPEC_3X3_S2 ? 4 : 0);
+      std::snprintf(tmp, sizeof tmp, "depthwise_f32_kernel<%d, %d, %s, %d>", k[dw_knob::VEC], k[dw_knob::RPT],
+                    tf(k[dw_knob::LDS]), spec);
+      break;
+    }
+    case CT_FAM_IGEMM_BF16:
+      std::snprintf(tmp, sizeof tmp, "igemm_bf16_kernel<%d, %d, %d, %s>", k[bf16_knob::MF], k[bf16_knob::TM],
+                    k[bf16_knob::TN], tf(k[bf16_knob::LDS]));
+      break;
+    default:
+      std::snprintf(tmp, sizeof tmp, "igemm_f32_kernel<%d, %d, %d, %d, %d>", k[f32g_knob::MF], k[f32g_knob::TM],
+                    k[f32g_knob::TN], k[f32g_knob::STAGES], (int)g.spec);
+  }
+  std::snprintf(buf, (size_t)cap, "%s", tmp);
   return CT_OK;
 }
 

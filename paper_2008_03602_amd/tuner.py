@@ -1,0 +1,253 @@
+"""Tuning runs over the C ABI: clients on CU slots, selection, cross-evaluation.
+
+This module only prepares inputs and marshals arguments; sampling, timing,
+selection and the client threads all run inside libconvtune.
+
+The paper's loop (section 2.1): select candidates (random with no history),
+build, profile on the device, pick the best. Its scaling (section 3.1.1):
+several profiling servers with fixed GPU shares, and a model's operators
+sharded over several tuning clients whose results are merged. Here a client
+is a library thread with its own CU-masked stream; the operators of a model
+are dealt to the clients round-robin, and the merged result is the per-layer
+winner. Cross-evaluation (section 2.2.1, Tables 1-2) re-runs the schedule
+tuned at one share on every other share.
+"""
+from __future__ import annotations
+
+import ctypes
+import json
+import time
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib as L
+from . import synth
+from . import workloads as W
+
+PEAK_FP32_TFLOPS = 157.3      # MI355X vector / matrix fp32, 256 CUs at 2.4 GHz
+PEAK_BF16_TFLOPS = 2516.6     # dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0
+
+
+@dataclass
+class LayerData:
+    """Device buffers of one layer: seeded synthetic x and w, an output y."""
+    op: W.Op
+    layer_id: int
+    x: torch.Tensor
+    w: torch.Tensor
+    y: torch.Tensor
+
+
+def make_layer(op: W.Op, cfg: W.TuneConfig, layer_id: int, device: str = "cuda:0") -> LayerData:
+    bf16 = op.dtype == W.DT_BF16
+    x, w = synth.conv_inputs(op.x_shape(), op.w_shape(), cfg.dist, cfg.seed, cfg.config_id, layer_id, bf16=bf16)
+    if bf16:
+        xd = torch.from_numpy(synth.bf16_bits(x).view(np.int16).copy()).to(device)
+        wd = torch.from_numpy(synth.bf16_bits(w).view(np.int16).copy()).to(device)
+    else:
+        xd = torch.from_numpy(x).to(device)
+        wd = torch.from_numpy(w).to(device)
+    yd = torch.empty(op.y_shape(), dtype=torch.float32, device=device)
+    return LayerData(op, layer_id, xd, wd, yd)
+
+
+@dataclass
+class JobResult:
+    op: W.Op
+    layer_id: int
+    client: int
+    fraction: float
+    candidates: List[L.ct_schedule]
+    lat1: np.ndarray
+    status1: np.ndarray
+    top_pos: np.ndarray
+    lat2: np.ndarray
+    winner_pos: int
+    winner_lat_us: float
+    t_start: float
+    t_end: float
+
+    @property
+    def winner(self) -> Optional[L.ct_schedule]:
+        return self.candidates[self.winner_pos] if self.winner_pos >= 0 else None
+
+    def summary(self) -> dict:
+        s = self.winner
+        d = {"layer": self.op.name, "client": self.client, "fraction": self.fraction,
+             "n_candidates": len(self.candidates),
+             "n_ok": int(np.sum(self.status1 == L.S_OK)),
+             "status_counts": {L.STATUS_NAMES[k]: int(np.sum(self.status1 == k)) for k in L.STATUS_NAMES
+                               if np.any(self.status1 == k)},
+             "winner_pos": self.winner_pos, "winner_lat_us": self.winner_lat_us,
+             "t_start": self.t_start, "t_end": self.t_end}
+        if s is not None:
+            d["winner"] = describe_schedule(self.op, s)
+            d["winner_tflops"] = self.op.flops() / (self.winner_lat_us * 1e-6) / 1e12
+            d["winner_gbps"] = self.op.bytes_moved() / (self.winner_lat_us * 1e-6) / 1e9
+        return d
+
+
+def describe_schedule(op: W.Op, s: L.ct_schedule) -> dict:
+    nk, _ = L.ct_grid_info(s.family)
+    names = {1: ["toh", "tow", "tk", "mk", "mw", "lds", "ct", "split", "unroll"],
+             2: ["tc", "toh", "tow", "vec", "rpt", "lds", "nb", "order"],
+             3: ["mfma", "tm", "tn", "wm", "wn", "kc", "lds", "split", "swizzle"],
+             4: ["mfma", "tm", "tn", "wm", "wn", "ws", "tpw", "cpc", "stages", "split"]}[s.family]
+    d = {"family": W.FAMILY_NAMES[s.family], "knobs": {names[i]: int(s.knob[i]) for i in range(nk)},
+         "grid_index": L.ct_grid_encode(s)}
+    d.update(L.ct_launch_shape(op, s))
+    return d
+
+
+class _Keep:
+    """Holds numpy/ctypes buffers alive for the duration of a library call."""
+
+    def __init__(self):
+        self.items = []
+
+    def add(self, x):
+        self.items.append(x)
+        return x
+
+
+def tune_clients(assignments: Sequence[Sequence[LayerData]], masks: Sequence[np.ndarray],
+                 cands: Dict[int, List[L.ct_schedule]], cfg: W.TuneConfig, fraction: float,
+                 verify_refs: Optional[Dict[int, torch.Tensor]] = None, verify_tol: float = 1e-4,
+                 pin_cores: bool = True, batch: int = 16) -> List[JobResult]:
+    """Run one client per assignment, concurrently, each on its CU mask.
+
+    assignments[j] lists the layers of client j; cands[layer_id] is that
+    layer's candidate list (sample order). Returns one JobResult per layer.
+    """
+    keep = _Keep()
+    clients = (L.ct_client * len(assignments))()
+    jobs_meta = []
+    for j, layers in enumerate(assignments):
+        jobs = keep.add((L.ct_tune_job * max(len(layers), 1))())
+        for i, ld in enumerate(layers):
+            c = cands[ld.layer_id]
+            arr = keep.add(L.schedule_array(c))
+            n = len(c)
+            lat1 = keep.add(np.zeros(max(n, 1), np.float32))
+            st1 = keep.add(np.zeros(max(n, 1), np.int32))
+            top = keep.add(np.zeros(cfg.top_t, np.int32))
+            lat2 = keep.add(np.zeros(cfg.top_t, np.float32))
+            jb = jobs[i]
+            jb.op = L.make_op(ld.op)
+            jb.x, jb.w, jb.y = ld.x.data_ptr(), ld.w.data_ptr(), ld.y.data_ptr()
+            jb.cands, jb.n_cands = arr, n
+            if verify_refs is not None and ld.layer_id in verify_refs:
+                jb.verify = L.ct_verify(verify_refs[ld.layer_id].data_ptr(), verify_tol)
+            jb.lat1_us = lat1.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+            jb.status1 = st1.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+            jb.top_t = cfg.top_t
+            jb.top_pos = top.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+            jb.lat2_us = lat2.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+            jobs_meta.append((j, i, ld, c, lat1, st1, top, lat2))
+        cl = clients[j]
+        for k, v in enumerate(masks[j]):
+            cl.cu_mask[k] = int(v)
+        cl.host_core = j if pin_cores else -1
+        cl.jobs = ctypes.cast(jobs, ctypes.POINTER(L.ct_tune_job))
+        cl.n_jobs = len(layers)
+        keep.add(jobs)
+    o1 = L.opts_from_protocol(cfg.stage1, batch=batch)
+    o2 = L.opts_from_protocol(cfg.stage2, batch=cfg.top_t, interleave=1)
+    L.ct_tune_clients(clients, o1, o2, cfg.eps)
+    out = []
+    for (j, i, ld, c, lat1, st1, top, lat2) in jobs_meta:
+        jb = ctypes.cast(clients[j].jobs, ctypes.POINTER(L.ct_tune_job))[i]
+        n, nt = len(c), jb.n_top
+        out.append(JobResult(ld.op, ld.layer_id, j, fraction, list(c), lat1[:n].copy(), st1[:n].copy(),
+                             top[:nt].copy(), lat2[:nt].copy(), jb.winner_pos, jb.winner_lat_us,
+                             jb.t_start_s, jb.t_end_s))
+    return out
+
+
+def round_robin(layers: Sequence[LayerData], k: int) -> List[List[LayerData]]:
+    """Shard a model's layers over k clients in table order (layer i -> client i mod k)."""
+    return [[ld for i, ld in enumerate(layers) if i % k == j] for j in range(k)]
+
+
+def cross_eval(ld: LayerData, winners: Sequence[L.ct_schedule], masks: Sequence[np.ndarray],
+               proto: W.Protocol, batch: int = 8) -> np.ndarray:
+    """M[i][j]: latency (us) of winners[i] on masks[j], repeats interleaved."""
+    o = L.opts_from_protocol(proto, batch=batch, interleave=1)
+    return L.ct_cross_eval(ld.op, winners, masks, o, ld.x, ld.w, ld.y)
+
+
+def throughput(n_candidates: int, t_first_start: float, t_last_end: float) -> float:
+    """Candidates per second over the makespan (first start to last end)."""
+    span = t_last_end - t_first_start
+    return n_candidates / span if span > 0 else float("nan")
+
+
+def sample_all(layers: Sequence[LayerData], cfg: W.TuneConfig) -> Dict[int, List[L.ct_schedule]]:
+    return {ld.layer_id: L.ct_sample(ld.op, cfg.seed, cfg.config_id, ld.layer_id, cfg.n_candidates)
+            for ld in layers}
+
+
+def tune_model_at_fraction(layers: Sequence[LayerData], cands, cfg: W.TuneConfig, fraction: float,
+                           clients: Optional[int] = None, **kw) -> List[JobResult]:
+    """Tune every layer at CU share `fraction`, with as many concurrent clients as
+    disjoint slots of that share fit on the device (or `clients`)."""
+    k = clients or max(1, int(round(1.0 / fraction)))
+    k = min(k, len(layers))
+    masks = [L.ct_cu_mask(fraction, j) for j in range(k)]
+    return tune_clients(round_robin(layers, k), masks, cands, cfg, fraction, **kw)
+
+
+def fraction_report(results: Sequence[JobResult]) -> dict:
+    t0 = min(r.t_start for r in results)
+    t1 = max(r.t_end for r in results)
+    n = sum(len(r.candidates) for r in results)
+    return {"candidates": n, "seconds": t1 - t0, "candidates_per_s": throughput(n, t0, t1),
+            "clients": len({r.client for r in results})}
+
+
+def main(argv=None) -> int:
+    import argparse
+    ap = argparse.ArgumentParser(description="Run a tuning configuration (1-5) and write a JSON report.")
+    ap.add_argument("--config", type=int, required=True)
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--clients", type=int, default=None)
+    ap.add_argument("--layers", type=int, default=None, help="only the first N layers")
+    ap.add_argument("--candidates", type=int, default=None)
+    a = ap.parse_args(argv)
+    cfg = W.config(a.config)
+    if a.candidates:
+        cfg.n_candidates = a.candidates
+    ops = cfg.ops[:a.layers] if a.layers else cfg.ops
+    L.ct_init(0)
+    layers = [make_layer(op, cfg, i) for i, op in enumerate(ops)]
+    cands = sample_all(layers, cfg)
+    report = {"config": cfg.describe(), "fractions": {}}
+    winners = {}
+    for f in cfg.fractions:
+        res = tune_model_at_fraction(layers, cands, cfg, f, clients=a.clients)
+        report["fractions"][str(f)] = {"throughput": fraction_report(res),
+                                       "layers": [r.summary() for r in res]}
+        for r in res:
+            winners.setdefault(r.layer_id, {})[f] = r.winner
+        print("fraction %.3f: %s" % (f, json.dumps(report["fractions"][str(f)]["throughput"])), flush=True)
+    if len(cfg.fractions) > 1:
+        masks = [L.ct_cu_mask(f, 0) for f in cfg.fractions]
+        report["cross_eval"] = {}
+        for ld in layers:
+            ws = [winners[ld.layer_id][f] for f in cfg.fractions]
+            if any(s is None for s in ws):
+                continue
+            M = cross_eval(ld, ws, masks, cfg.stage2)
+            report["cross_eval"][ld.op.name] = M.tolist()
+    if a.out:
+        with open(a.out, "w") as fh:
+            json.dump(report, fh, indent=1)
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())
