@@ -33,17 +33,27 @@ FRACTIONS = (0.25, 0.5, 1.0)
 HEADLINE = "r18.2"
 
 
-def cpu_baseline(cfg, budget_s: float = 20.0) -> dict:
-    """The fp64 oracle timed on this host on a bounded sample of the workload."""
-    import numpy as np
+def runs_per_candidate(cfg, n_layers: int, n_fractions: int) -> float:
+    """Convolution launches one step makes per screened candidate: the screen,
+    the top-T re-measure and the cross-evaluation, over all layers and shares."""
+    p1, p2 = cfg.stage1, cfg.stage2
+    screen = cfg.n_candidates * (p1.warmup + p1.repeats * p1.launches)
+    remeasure = cfg.top_t * (p2.warmup + p2.repeats * p2.launches)
+    cross = n_fractions * n_fractions * (p2.warmup + p2.repeats * p2.launches)
+    runs = n_layers * (n_fractions * (screen + remeasure) + cross)
+    return runs / (n_layers * n_fractions * cfg.n_candidates)
 
+
+def cpu_baseline(cfg, runs_per_cand: float, budget_s: float = 20.0) -> dict:
+    """The fp64 oracle timed on this host on a bounded sample of the workload.
+
+    One oracle convolution stands in for one convolution launch of the tuner, so
+    candidates/s = oracle convolutions/s / (launches per screened candidate)."""
     import oracle
     from paper_2008_03602_amd import synth
 
     threads = len(os.sched_getaffinity(0))
     done, flops, t_total = 0, 0, 0.0
-    names = []
-    # one oracle evaluation per layer stands in for one candidate evaluation;
     # the layer list is walked round-robin until the time budget is used
     while t_total < budget_s and done < 50 * len(cfg.ops):
         op = cfg.ops[done % len(cfg.ops)]
@@ -53,12 +63,14 @@ def cpu_baseline(cfg, budget_s: float = 20.0) -> dict:
         oracle.conv2d(x, w, (op.stride_h, op.stride_w), (op.pad_h, op.pad_w), threads=threads)
         t_total += time.perf_counter() - t0
         flops += op.flops()
-        names.append(op.name)
         done += 1
-    return {"value": done / t_total, "unit": "oracle conv evaluations/s", "cores": threads,
-            "kind": "oracle", "gflops": flops / t_total / 1e9, "seconds": t_total,
-            "sample": "%d fp64 oracle convolutions over the ResNet-18 layer list (%s), OpenMP over "
-                      "(n, k) on %d threads" % (done, ",".join(names), threads)}
+    convs = done / t_total
+    return {"value": convs / runs_per_cand, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "oracle_convs_per_s": convs, "gflops": flops / t_total / 1e9, "seconds": t_total,
+            "sample": "%d fp64 oracle convolutions at full size, the %d ResNet-18 b1 layers in turn "
+                      "(%.1f passes over the list), %.1f s on %d threads; candidates/s = convolutions/s "
+                      "divided by the %.1f convolution launches the GPU step makes per screened candidate"
+                      % (done, len(cfg.ops), done / len(cfg.ops), t_total, threads, runs_per_cand)}
 
 
 def main() -> int:
@@ -98,11 +110,20 @@ def main() -> int:
                 cross[ld.op.name] = T.cross_eval(ld, winners, masks, cfg.stage2)
         return res, cross
 
-    for _ in range(a.warmup):
+    def progress(what, t):
+        print("[bench] %s done in %.1f s" % (what, time.perf_counter() - t), file=sys.stderr, flush=True)
+
+    for i in range(a.warmup):
+        tw = time.perf_counter()
         step()
+        progress("warm-up step %d/%d" % (i + 1, a.warmup), tw)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    steps = [step() for _ in range(a.steps)]
+    steps = []
+    for i in range(a.steps):
+        ts = time.perf_counter()
+        steps.append(step())
+        progress("timed step %d/%d" % (i + 1, a.steps), ts)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     res, cross = steps[-1]
@@ -129,6 +150,11 @@ def main() -> int:
     r100 = head[1.0]
     ach = op.flops() / (r100.winner_lat_us * 1e-6) / 1e12
     fr = {f: T.fraction_report(res[f]) for f in FRACTIONS}
+    # HBM bytes per launch of this kernel and shape from committed counter
+    # runs, if the kernel's sources are unchanged since they were taken
+    from paper_2008_03602_amd import profsum
+    tblk = profsum.find_traffic(os.path.join(ROOT, "profiles"), per_fraction[-1]["kernel"],
+                                per_fraction[-1]["schedule"])
     line = {
         "metric": "tuning candidates measured/sec (1 GPU); best conv2d TFLOP/s and % roofline per CU fraction",
         "value": value, "unit": "candidates/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
@@ -144,7 +170,10 @@ def main() -> int:
         "per_fraction_throughput": {str(f): fr[f] for f in FRACTIONS},
         "roofline": {"bound": "mfma" if "igemm" in per_fraction[-1]["kernel"] else "alu",
                      "achieved": ach, "peak": T.PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-                     "frac": ach / T.PEAK_FP32_TFLOPS, "traffic": None,
+                     "frac": ach / T.PEAK_FP32_TFLOPS,
+                     "traffic": tblk["traffic_bytes"] if tblk else None,
+                     "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "algorithmic_bytes_per_launch": op.bytes_moved(),
                      "kernel": per_fraction[-1]["kernel"], "layer": HEADLINE,
                      "flops_per_launch": op.flops(), "latency_us": r100.winner_lat_us,
                      "launch_shape": per_fraction[-1]["schedule"]},
@@ -158,8 +187,10 @@ def main() -> int:
         with open(a.report, "w") as fh:
             json.dump(rep, fh, indent=1)
     if not a.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg)
+        line["cpu_baseline"] = cpu_baseline(cfg, runs_per_candidate(cfg, len(layers), len(FRACTIONS)))
     print(json.dumps(line), flush=True)
+    torch.cuda.synchronize()
+    L.ct_shutdown()  # release the library's streams and events before interpreter exit
     return 0
 
 

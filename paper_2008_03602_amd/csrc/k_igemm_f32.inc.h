@@ -47,8 +47,16 @@ struct IgF32Args {
   int bm, bn, threads;
   int cps, chunks;
   int n_halo, n_filt;  // staged halo / filter elements per thread per chunk
+  // host-precomputed: exact reciprocals for small quotients, and the block
+  // size decomposed over the halo (c, hh, ww) and filter (m, c, tap) indices
+  float inv_plane, inv_wt, inv_perm, inv_rs, inv_tpw;
+  int h_dc, h_dhh, h_dww, f_dm, f_dc, f_dtap;
   int64_t ny;
 };
+
+// floor(n / d) for 0 <= n < 2^22 given inv = 1/d in fp32: (n + 1/2)/d lies at
+// least 1/(2d) from an integer and the fp32 product errs by less than that.
+__device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
 
 __host__ __device__ constexpr int ig_spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
 __host__ __device__ constexpr int ig_spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
@@ -125,20 +133,21 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   // i.e. 0) and stores to LDS (an unused slot into a per-lane dummy word), so
   // the staging code has no branches and all loads are in flight at once.
   const int dummy = STAGES * stage_floats + lane;
+  // channels of x per chunk: CPC divides C, or one chunk holds all C (< CPC)
+  const int cl = min(a.cpc, a.C);
   int s_off[kF32Slots], s_lds[kF32Slots];
   {
     // halo element e = t + i*threads of Xs[cpcp][ht][wt] -> (c, hh, ww)
     const int T = a.threads;
-    int c = t / plane, rem = t - c * plane;
-    int hh = rem / wt, ww = rem - hh * wt;
-    const int dc = T / plane, drem = T - dc * plane;
-    const int dhh = drem / wt, dww = drem - dhh * wt;
+    int c = qdiv(t, a.inv_plane), rem = t - c * plane;
+    int hh = qdiv(rem, a.inv_wt), ww = rem - hh * wt;
+    const int dc = a.h_dc, dhh = a.h_dhh, dww = a.h_dww;
 #pragma unroll
     for (int i = 0; i < kF32Slots; ++i) {
       if (i < a.n_halo) {
         const int gh = ih0 + hh, gw = iw0 + ww;
         const int e = t + i * T;
-        const bool ok = c < a.cpc && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
+        const bool ok = c < cl && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
         s_off[i] = ok ? ((nimg * a.C + c) * HW + gh * a.W + gw) * 4 : kOob;
         s_lds[i] = e < xs_floats ? e : -1;
         ww += dww;
@@ -152,17 +161,16 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   {
     // filter element e = t + j*threads of the chunk's BM x CPCP x RS slice, in
     // global order (m, c, tap); LDS position m*lda + tap*cpcp + c
-    const int T = a.threads, per_m = cpcp * RS;
-    int m = t / per_m, rem = t - m * per_m;
-    int c = rem / RS, tap = rem - c * RS;
-    const int dm = T / per_m, drem = T - dm * per_m;
-    const int dcc = drem / RS, dtap = drem - dcc * RS;
+    const int per_m = cpcp * RS;
+    int m = qdiv(t, a.inv_perm), rem = t - m * per_m;
+    int c = qdiv(rem, a.inv_rs), tap = rem - c * RS;
+    const int dm = a.f_dm, dcc = a.f_dc, dtap = a.f_dtap;
 #pragma unroll
     for (int i = 0; i < kF32Slots; ++i) {
       const int j = i - a.n_halo;
       if (j >= 0 && j < a.n_filt) {
         const bool in_tile = m < bm;
-        const bool ok = in_tile && k0 + m < a.K && c < a.cpc;
+        const bool ok = in_tile && k0 + m < a.K && c < cl;
         s_off[i] = ok ? ((k0 + m) * a.kred + c * RS + tap) * 4 : kOob;
         s_lds[i] = in_tile ? xs_floats + m * lda + tap * cpcp + c : -1;
         tap += dtap;
@@ -176,22 +184,6 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       }
     }
   }
-  // A partial last chunk (C not a multiple of CPC) masks the channels it lacks;
-  // this runs once, before that chunk's loads are issued.
-  auto mask_missing_channels = [&](int cl) {
-#pragma unroll
-    for (int i = 0; i < kF32Slots; ++i) {
-      int c;
-      if (i < a.n_halo) {
-        c = (t + i * a.threads) / plane;
-      } else {
-        const int e = t + (i - a.n_halo) * a.threads;
-        c = (e % (cpcp * RS)) / RS;
-      }
-      if (c >= cl) s_off[i] = kOob;
-    }
-  };
-
   const int ch_begin = sp * a.cps;
   const int ch_end = min(a.chunks, ch_begin + a.cps);
   const int64_t xbytes = (int64_t)a.N * a.C * HW * 4, wbytes = (int64_t)a.K * a.kred * 4;
@@ -199,7 +191,6 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   float rv[kF32Slots];
   auto load_chunk = [&](int ch) {
     const int c0 = ch * a.cpc;
-    if (c0 + a.cpc > a.C) mask_missing_channels(a.C - c0);
     // descriptors start at the chunk's first channel
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)c0 * HW, xbytes - (int64_t)c0 * HW * 4);
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)c0 * RS, wbytes - (int64_t)c0 * RS * 4);
@@ -228,37 +219,38 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int q = n_off + j * MF + lrow;
-    const int pr = q / a.tpw, pc = q - pr * a.tpw;
+    const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
     b_base[j] = kg * plane + (pr * sh) * wt + pc * sw;
   }
   const int n_i = cpcp / KSTEP / a.wsp;  // k-steps per tap for this reduction group
   const int i_begin = wg * n_i;
+  // For each tap, the reduction group's channel steps run in groups of 4:
+  // all fragment reads of a group are issued before its MFMAs.
   auto compute = [&](int stage) {
     const float* Xs = smem + stage * stage_floats;
     const float* As = Xs + xs_floats;
     for (int r = 0; r < R; ++r) {
       for (int s = 0; s < S; ++s) {
-        const int tap = r * S + s;
-        const float* ap = As + tap * cpcp + i_begin * KSTEP;
+        const float* ap = As + (r * S + s) * cpcp + i_begin * KSTEP;
         const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * KSTEP * plane;
         int ii = 0;
-        for (; ii + 2 <= n_i; ii += 2) {
-          float fa[2][TM], fb[2][TN];
+        for (; ii + 4 <= n_i; ii += 4) {
+          float fa[4][TM], fb[4][TN];
 #pragma unroll
-          for (int u = 0; u < 2; ++u) {
+          for (int u = 0; u < 4; ++u) {
 #pragma unroll
             for (int i = 0; i < TM; ++i) fa[u][i] = ap[a_base[i] + (ii + u) * KSTEP];
 #pragma unroll
             for (int j = 0; j < TN; ++j) fb[u][j] = bp[b_base[j] + (ii + u) * KSTEP * plane];
           }
 #pragma unroll
-          for (int u = 0; u < 2; ++u)
+          for (int u = 0; u < 4; ++u)
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
               for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[u][i], fb[u][j], acc[i][j]);
         }
-        if (ii < n_i) {
+        for (; ii < n_i; ++ii) {
           float fa[TM], fb[TN];
 #pragma unroll
           for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * KSTEP];
@@ -324,19 +316,20 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   }
 
   float* o = out + (int64_t)sp * a.ny;
+  const int ohw = a.OH * a.OW;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int q = n_off + j * MF + lrow;
-    const int pr = q / a.tpw, pc = q - pr * a.tpw;
+    const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
     const int oh = oh0 + pr, ow = ow0 + pc;
     if (oh >= a.OH || ow >= a.OW) continue;
-    float* op = o + ((int64_t)nimg * a.K * a.OH + oh) * a.OW + ow;
+    const int base = (nimg * a.K + k0 + m_off) * ohw + oh * a.OW + ow;  // y offset of channel k0+m_off
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int e = 0; e < ACC; ++e) {
-        const int k = k0 + m_off + i * MF + M::row(e, lane);
-        if (k < a.K) op[(int64_t)k * a.OH * a.OW] = acc[i][j][e];
+        const int kr = i * MF + M::row(e, lane);
+        if (k0 + m_off + kr < a.K) o[base + kr * ohw] = acc[i][j][e];
       }
     }
   }

@@ -306,6 +306,8 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   if (tpw > fit_pow2(x.ow, 8, 64)) REJECT("pixel tile wider than the output");
   if (tph > fit_pow2(x.oh, 1, 1024)) REJECT("pixel tile taller than the output");
   if (cpc > fit(f.knobs[CPC], x.cg)) REJECT("channels per chunk exceed C");
+  // every chunk holds the same channels: no partial last chunk to mask
+  if (cpc < x.cg && x.cg % cpc) REJECT("channels per chunk do not divide C");
   const int acc_regs = tm * tn * (mf == 32 ? 16 : 4);
   if (acc_regs > 128) REJECT("accumulator tile too large");
   const int threads = 64 * wm * wn * wsplit;

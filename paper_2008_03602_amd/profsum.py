@@ -1,0 +1,318 @@
+"""Summarise rocprofv3 output: per-kernel statistics, the bench's roofline
+kernel, and HBM traffic from FETCH_SIZE / WRITE_SIZE counter runs.
+
+Usage:
+  python -m paper_2008_03602_amd.profsum --trace DIR [--bench FILE] [--replay FILE]
+      [--fetch DIR --write DIR] [--out profiles/x.md] [--cmd "..."]...
+
+--trace DIR   rocprofv3 --kernel-trace output: a rocpd database (``*.db``, the
+              default format) or ``*kernel_trace.csv`` (``-f csv``).
+--bench FILE  a file holding bench.py's JSON line: the roofline kernel's
+              dispatches are picked out of the trace by name, workgroup size and
+              total grid size, and their average duration is set beside the
+              latency bench.py measured with HIP events.
+--replay FILE the JSON line of ``tuner --replay`` (the same kernel run alone,
+              then the copy kernel over a known number of bytes).
+--fetch/--write DIR  ``-f csv`` output of a ``--pmc FETCH_SIZE`` and a
+              ``--pmc WRITE_SIZE`` run of that replay. The counters read KiB per
+              dispatch; each is scaled by known bytes / counted bytes of the copy
+              kernel in the same run.
+
+The output ends with a JSON block (``traffic``) that bench.py reads back: it
+names the kernel, its launch shape and a hash of the kernel's source files, so
+a later change to the kernel voids the figure.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import sqlite3
+import statistics
+import sys
+from collections import defaultdict
+
+CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+
+# kernel name prefix -> the source files that define it
+_KERNEL_SOURCES = {
+    "direct_f32_kernel": ["k_direct*"],
+    "depthwise_f32_kernel": ["k_depthwise*"],
+    "igemm_bf16_kernel": ["k_igemm_bf16*"],
+    "igemm_f32_kernel": ["k_igemm_f32*"],
+}
+
+
+def kernel_source_hash(kernel: str) -> str | None:
+    """sha256 over the sources of the family that `kernel` belongs to, plus the
+    shared headers; None for a kernel this library does not define."""
+    base = kernel.replace("void ", "").split("<")[0].split("(")[0].split("::")[-1]
+    pats = _KERNEL_SOURCES.get(base)
+    if not pats:
+        return None
+    files = sorted(set(f for p in pats + ["k_util.h", "ct_internal.h"] for f in glob.glob(os.path.join(CSRC, p))))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def short_name(name: str) -> str:
+    return name.replace("void ", "").split("(")[0]
+
+
+# ---------------------------------------------------------------- trace input
+class Trace:
+    """Kernel dispatches of one profiler run: (name, grid items, wg size, duration ns)."""
+
+    def __init__(self, directory: str):
+        dbs = sorted(glob.glob(os.path.join(directory, "**", "*.db"), recursive=True))
+        self.db = sqlite3.connect(dbs[0]) if dbs else None
+        self.rows = None
+        if self.db is None:
+            self.rows = []
+            for path in sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True)):
+                with open(path) as fh:
+                    for r in csv.DictReader(fh):
+                        grid = _int(r, "Grid_Size") or (_int(r, "Grid_Size_X") * max(_int(r, "Grid_Size_Y"), 1)
+                                                        * max(_int(r, "Grid_Size_Z"), 1))
+                        wg = _int(r, "Workgroup_Size") or (_int(r, "Workgroup_Size_X")
+                                                           * max(_int(r, "Workgroup_Size_Y"), 1)
+                                                           * max(_int(r, "Workgroup_Size_Z"), 1))
+                        self.rows.append((r.get("Kernel_Name", ""), grid, wg, _int(r, "LDS_Block_Size", "Lds_Size"),
+                                          _int(r, "End_Timestamp") - _int(r, "Start_Timestamp")))
+
+    def by_stream(self, kernel: str, wg: int | None, grid: int | None, lds: int | None = None):
+        """{stream id: [durations]} of the matching dispatches (rocpd traces only)."""
+        out = defaultdict(list)
+        if self.db is None:
+            return out
+        q = ("SELECT name, workgroup_x * workgroup_y * workgroup_z, grid_x * grid_y * grid_z, lds_size, "
+             "stream_id, duration FROM kernels WHERE name LIKE ?")
+        for n, w, g, l, st, d in self.db.execute(q, ("%" + kernel + "%",)):
+            if (kernel in n.replace("void ", "") and (wg is None or w == wg) and (grid is None or g == grid)
+                    and (lds is None or l == lds)):
+                out[st].append(d)
+        return out
+
+    def per_kernel(self):
+        """[(short name, dispatches, total ns, mean ns)] sorted by total time."""
+        by = defaultdict(lambda: [0, 0])
+        if self.db is not None:
+            q = "SELECT name, count(*), sum(duration) FROM kernels GROUP BY name"
+            for name, n, tot in self.db.execute(q):
+                e = by[short_name(name)]
+                e[0] += n
+                e[1] += tot
+        else:
+            for name, _, _, _, d in self.rows:
+                e = by[short_name(name)]
+                e[0] += 1
+                e[1] += d
+        out = [(k, n, tot, tot / n) for k, (n, tot) in by.items()]
+        return sorted(out, key=lambda r: -r[2])
+
+    def durations(self, kernel: str, wg: int | None, grid: int | None, lds: int | None = None):
+        """Durations (ns) of the dispatches of `kernel` with that shape (and LDS bytes)."""
+        if self.db is not None:
+            q = ("SELECT name, workgroup_x * workgroup_y * workgroup_z, grid_x * grid_y * grid_z, lds_size, "
+                 "duration FROM kernels WHERE name LIKE ?")
+            rows = self.db.execute(q, ("%" + kernel + "%",)).fetchall()
+        else:
+            rows = [(n, w, g, l, d) for n, g, w, l, d in self.rows if kernel in n]
+        return [d for n, w, g, l, d in rows
+                if kernel in n.replace("void ", "") and (wg is None or w == wg) and (grid is None or g == grid)
+                and (lds is None or l == lds)]
+
+
+def _int(r, *names):
+    for n in names:
+        if n in r and r[n] not in (None, ""):
+            return int(float(r[n]))
+    return 0
+
+
+def counter_per_dispatch(directory: str, counter: str):
+    """{short kernel name: [value per dispatch]} from a --pmc CSV run."""
+    out = defaultdict(list)
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
+        with open(path) as fh:
+            per = defaultdict(float)
+            names = {}
+            for r in csv.DictReader(fh):
+                if r.get("Counter_Name") != counter:
+                    continue
+                key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+                per[key] += float(r["Counter_Value"])
+                names[key] = r.get("Kernel_Name", "")
+            for key, v in per.items():
+                out[short_name(names[key])].append(v)
+    return out
+
+
+# ---------------------------------------------------------------- summary
+def _read_json_line(path: str, key: str):
+    if not path:
+        return None
+    with open(path) as fh:
+        for line in fh:
+            line = line.strip()
+            if line.startswith("{") and key in line:
+                return json.loads(line)
+    return None
+
+
+def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None, cmds=()) -> str:
+    tr = Trace(trace_dir)
+    lines = ["# rocprofv3 kernel summary", ""]
+    if tr.db is None and not tr.rows:
+        lines += ["No trace (no rocpd database or kernel_trace.csv) under %s." % trace_dir, ""]
+    if cmds:
+        lines += ["Commands (run from the repository root):", "", "```"] + list(cmds) + ["```", ""]
+    rows = tr.per_kernel()
+    total = sum(r[2] for r in rows)
+    lines += ["Trace: %d dispatches, total kernel time %.3f ms." % (sum(r[1] for r in rows), total / 1e6), "",
+              "| kernel | dispatches | total ms | share | avg us |", "|---|---|---|---|---|"]
+    for name, n, tot, mean in rows[:25]:
+        lines.append("| `%s` | %d | %.3f | %.1f%% | %.2f |" % (name, n, tot / 1e6, 100.0 * tot / max(total, 1),
+                                                                mean / 1e3))
+    block = {}
+    if bench and "roofline" in bench:
+        rf = bench["roofline"]
+        shape = rf.get("launch_shape", {})
+        kname = rf.get("kernel", "")
+        threads, blocks = shape.get("threads"), shape.get("blocks")
+        grid = blocks * threads if blocks and threads else None
+        durs = tr.durations(kname, threads, grid, shape.get("lds_bytes"))
+        lines += ["", "## Roofline kernel", "",
+                  "bench.py names `%s` (layer %s, %s blocks x %s threads, LDS %s bytes), %.3f GFLOP per launch."
+                  % (kname, rf.get("layer"), blocks, threads, shape.get("lds_bytes"),
+                     rf.get("flops_per_launch", 0) / 1e9), ""]
+        if durs:
+            avg = statistics.mean(durs) / 1e3
+            groups = tr.by_stream(kname, threads, grid, shape.get("lds_bytes"))
+            if len(groups) > 1:
+                # the same candidate list is timed on every CU share: one stream per share
+                lines += ["The kernel ran on %d streams (one per CU share and client); per stream:" % len(groups),
+                          "", "| stream | launches | avg us |", "|---|---|---|"]
+                for st, v in sorted(groups.items(), key=lambda kv: statistics.mean(kv[1])):
+                    lines.append("| %s | %d | %.3f |" % (st, len(v), statistics.mean(v) / 1e3))
+                durs = min(groups.values(), key=statistics.mean)
+                lines += ["", "The fastest streams are the full-GPU ones (the roofline's share); the rows below "
+                              "use the fastest.", ""]
+                avg = statistics.mean(durs) / 1e3
+            if shape.get("kernels", 1) > 1:
+                red = tr.durations("split_reduce_kernel", None, None)
+                lines += ["The schedule splits the reduction, so bench.py's latency covers this kernel plus "
+                          "`split_reduce_kernel`; the trace holds %d launches of the latter from all split "
+                          "schedules (avg %.3f us)." % (len(red), statistics.mean(red) / 1e3 if red else 0.0), ""]
+            lines += ["| source | launches | avg us | median us |", "|---|---|---|---|",
+                      "| rocprofv3 kernel trace | %d | %.3f | %.3f |" % (len(durs), avg,
+                                                                      statistics.median(durs) / 1e3),
+                      "| bench.py HIP events (median of repeat means) | - | %.3f | - |" % rf.get("latency_us", 0.0),
+                      "", "From the trace average: %.2f TFLOP/s, %.1f%% of %.1f %s." % (
+                          rf["flops_per_launch"] / (avg * 1e-6) / 1e12,
+                          100.0 * rf["flops_per_launch"] / (avg * 1e-6) / 1e12 / rf["peak"], rf["peak"],
+                          rf.get("unit", ""))]
+            lines.append("(The bench's first launch of each repeat follows a host-side event record, so "
+                         "its HIP-event mean also holds launch gaps that the trace does not.)")
+        else:
+            lines.append("No dispatch of that kernel with that shape is in the trace.")
+    if replay:
+        lines += ["", "## Replay (kernel alone)", "",
+                  "`%s`, %d launches at %.0f%% of the CUs: %.3f us by HIP events, %.2f TFLOP/s." % (
+                      replay["kernel"], replay["launches"], 100 * replay["fraction"], replay["latency_us"],
+                      replay["tflops"])]
+        sh = replay["schedule"]
+        rdurs = tr.durations(replay["kernel"], sh.get("threads"), sh.get("blocks", 0) * sh.get("threads", 0),
+                             sh.get("lds_bytes"))
+        if rdurs:
+            lines.append("Trace of the replay: %d launches, avg %.3f us, median %.3f us." % (
+                len(rdurs), statistics.mean(rdurs) / 1e3, statistics.median(rdurs) / 1e3))
+            if sh.get("kernels", 1) > 1:
+                red = tr.durations("split_reduce_kernel", None, None)
+                if red:
+                    both = statistics.mean(rdurs) + statistics.mean(red)
+                    lines.append("The schedule splits the reduction: each run is the kernel above plus "
+                                 "`split_reduce_kernel` (avg %.3f us over %d launches), %.3f us together "
+                                 "(%.2f TFLOP/s)." % (statistics.mean(red) / 1e3, len(red), both / 1e3,
+                                                      replay["tflops"] * replay["latency_us"] / (both / 1e3)))
+    if replay and fetch_dir and write_dir:
+        k = short_name(replay["kernel"])
+        f = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
+        w = counter_per_dispatch(write_dir, "WRITE_SIZE")
+        kf = [v for name, vs in f.items() if k in name for v in vs]
+        kw = [v for name, vs in w.items() if k in name for v in vs]
+        cf = [v for name, vs in f.items() if "copy_kernel" in name for v in vs]
+        cw = [v for name, vs in w.items() if "copy_kernel" in name for v in vs]
+        nbytes = replay.get("copy_bytes_each_way", 0)
+        if kf and kw and cf and cw and nbytes:
+            sf = nbytes / (max(cf) * 1024.0)
+            sw = nbytes / (max(cw) * 1024.0)
+            fetch = statistics.median(kf) * 1024.0 * sf
+            write = statistics.median(kw) * 1024.0 * sw
+            lines += ["", "## HBM traffic (counters)", "",
+                      "| counter | copy kernel KiB (known %d MiB) | scale | kernel KiB per launch (median of %d) "
+                      "| kernel bytes per launch |" % (nbytes >> 20, len(kf)),
+                      "|---|---|---|---|---|",
+                      "| FETCH_SIZE | %.0f | %.4f | %.1f | %.0f |" % (max(cf), sf, statistics.median(kf), fetch),
+                      "| WRITE_SIZE | %.0f | %.4f | %.1f | %.0f |" % (max(cw), sw, statistics.median(kw), write)]
+            sched = replay["schedule"]
+            block = {"kernel": replay["kernel"], "layer": replay["layer"], "threads": sched.get("threads"),
+                     "blocks": sched.get("blocks"), "lds_bytes": sched.get("lds_bytes"),
+                     "knobs": sched.get("knobs"), "fetch_bytes": fetch, "write_bytes": write,
+                     "traffic_bytes": fetch + write, "source_hash": kernel_source_hash(replay["kernel"])}
+        else:
+            lines += ["", "Counter runs incomplete: traffic not derived."]
+    if block:
+        lines += ["", "```json", json.dumps({"traffic": block}), "```"]
+    return "\n".join(lines) + "\n"
+
+
+def find_traffic(profiles_dir: str, kernel: str, shape: dict):
+    """Traffic bytes per launch for `kernel` with this launch shape from a
+    summary under profiles_dir, or None (no summary, another shape, or the
+    kernel's sources changed since the counters were taken)."""
+    want = kernel_source_hash(kernel)
+    for path in sorted(glob.glob(os.path.join(profiles_dir, "*.md"))):
+        text = open(path).read()
+        start = text.rfind("```json\n")
+        if start < 0:
+            continue
+        try:
+            blk = json.loads(text[start + 8:text.index("```", start + 8)])["traffic"]
+        except (ValueError, KeyError):
+            continue
+        if (blk.get("kernel") == kernel and blk.get("threads") == shape.get("threads")
+                and blk.get("blocks") == shape.get("blocks") and blk.get("knobs") == shape.get("knobs")
+                and want is not None and blk.get("source_hash") == want):
+            return blk
+    return None
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--bench", default=None, help="file holding bench.py's JSON line")
+    ap.add_argument("--replay", default=None, help="file holding tuner --replay's JSON line")
+    ap.add_argument("--fetch", default=None)
+    ap.add_argument("--write", default=None)
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--cmd", action="append", default=[])
+    a = ap.parse_args(argv)
+    text = summarize(a.trace, _read_json_line(a.bench, '"metric"'), _read_json_line(a.replay, '"kernel"'),
+                     a.fetch, a.write, a.cmd)
+    if a.out:
+        with open(a.out, "w") as fh:
+            fh.write(text)
+    sys.stdout.write(text)
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())

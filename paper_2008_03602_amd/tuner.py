@@ -209,15 +209,65 @@ def fraction_report(results: Sequence[JobResult]) -> dict:
             "clients": len({r.client for r in results})}
 
 
+def find_layer(name: str):
+    """(op, config, layer position) of a named layer of configurations 1-5."""
+    for cid in range(1, 6):
+        cfg = W.config(cid)
+        for i, op in enumerate(cfg.ops):
+            if op.name == name:
+                return op, cfg, i
+    raise KeyError("no layer named %r in configurations 1-5" % name)
+
+
+def replay(layer: str, family: int, knobs: Sequence[int], fraction: float, launches: int,
+           copy_mib: int) -> dict:
+    """Run one schedule of one layer `launches` times back to back on slot 0 of
+    `fraction`, then (if copy_mib > 0) the library's copy kernel over copy_mib
+    MiB, so that a profiler run sees the kernel alone next to a transfer of
+    known size."""
+    op, cfg, i = find_layer(layer)
+    ld = make_layer(op, cfg, i)
+    s = L.make_schedule(family, list(knobs))
+    if L.ct_validate(op, s) != 0:
+        raise ValueError("invalid schedule: " + L.ct_last_error())
+    mask = L.ct_cu_mask(fraction, 0)
+    lat, st = L.measure_candidates_mask(op, [s], mask, L.make_opts(1, 1, launches, 1), ld.x, ld.w, ld.y)
+    out = {"layer": layer, "kernel": L.ct_kernel_name(op, s), "schedule": describe_schedule(op, s),
+           "fraction": fraction, "launches": launches, "status": int(st[0]), "latency_us": float(lat[0]),
+           "tflops": op.flops() / (float(lat[0]) * 1e-6) / 1e12}
+    if copy_mib > 0:
+        n = copy_mib * (1 << 20)
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        out["copy_bytes_each_way"] = n
+        out["copy_gbps"] = L.ct_probe_copy(mask, src, dst, n, L.make_opts(1, 1, 1, 1))
+    torch.cuda.synchronize()
+    return out
+
+
 def main(argv=None) -> int:
     import argparse
-    ap = argparse.ArgumentParser(description="Run a tuning configuration (1-5) and write a JSON report.")
-    ap.add_argument("--config", type=int, required=True)
+    ap = argparse.ArgumentParser(description="Run a tuning configuration (1-5) and write a JSON report, "
+                                             "or replay one schedule (--replay).")
+    ap.add_argument("--config", type=int, default=None)
     ap.add_argument("--out", default=None)
     ap.add_argument("--clients", type=int, default=None)
     ap.add_argument("--layers", type=int, default=None, help="only the first N layers")
     ap.add_argument("--candidates", type=int, default=None)
+    ap.add_argument("--replay", default=None, metavar="LAYER:FAMILY:K0,K1,...",
+                    help="run one schedule of one layer and print its latency")
+    ap.add_argument("--fraction", type=float, default=1.0, help="CU share for --replay")
+    ap.add_argument("--launches", type=int, default=200, help="back-to-back launches for --replay")
+    ap.add_argument("--copy-mib", type=int, default=0, help="--replay: also run the copy kernel over this many MiB")
     a = ap.parse_args(argv)
+    if a.replay:
+        layer, fam, knobs = a.replay.split(":")
+        L.ct_init(0)
+        out = replay(layer, int(fam), [int(k) for k in knobs.split(",")], a.fraction, a.launches, a.copy_mib)
+        print(json.dumps(out), flush=True)
+        return 0 if out["status"] == L.S_OK else 1
+    if a.config is None:
+        ap.error("--config or --replay is required")
     cfg = W.config(a.config)
     if a.candidates:
         cfg.n_candidates = a.candidates
