@@ -3,31 +3,33 @@
 // K x C x R x S w, NCHW y.
 //
 // GEMM view: rows = output channels, columns = output pixels, reduction =
-// (filter tap, input channel). A block owns a BM x BN tile: BM = WM*TM*MF
+// (input channel, filter tap). A block owns a BM x BN tile: BM = WM*TM*MF
 // output channels by BN = WN*TN*MF output pixels, the pixels forming a
 // TPH x TPW rectangle of one image (TPW = the TPW knob, TPH = BN / TPW).
 //
 // Staging. The reduction advances one chunk of CPC input channels at a time
-// (padded to CPCP, a whole number of MFMA k-groups per reduction group). A
-// chunk stages in LDS
-//   * the input halo of the pixel rectangle, Xs[CPCP][HT][WT], loaded once:
-//     every filter tap reads its operand from this tile, so a 3x3 filter
-//     costs one global load per input element instead of nine;
-//   * the filter slice As[BM][R*S][CPCP] (row pitch LDA), tap-major so that
-//     consecutive MFMA k-steps are consecutive channels of one tap.
-// Global reads are raw buffer loads: the descriptor base advances one chunk
-// per iteration (scalar work); per-lane byte offsets are fixed for the whole
-// kernel, and an element that is padding, overhang or a padded channel gets
-// an offset beyond the buffer, which reads as 0. The staging plan is built
-// with carry counters (no per-element divisions).
+// (CPC divides C, or a single chunk holds all of C), padded to CPCP channels
+// so that every reduction group gets whole MFMA k-steps. A chunk stages in LDS
+//   * the input halo of the pixel rectangle, Xs[CPCP][HT][WT]: every filter
+//     tap reads its operand from this tile, so a 3x3 filter costs one global
+//     read per input element instead of nine;
+//   * the filter slice As[BM][CPCP*R*S] in global order, rows padded to an odd
+//     pitch LDA so that the rows one MFMA operand reads fall in distinct banks.
+// Both are copied by buffer loads that write LDS directly, without a round
+// trip through registers: one wave instruction fills 64 consecutive LDS
+// words, lane i the i-th. The halo is copied as a flat array; the lanes'
+// offsets into x are fixed for the whole kernel (built once, with carry
+// counters) and a padding element, a padded channel or a channel past the
+// chunk gets an offset that the buffer's range check turns into 0. The
+// filter is copied 64 words of a row at a time.
 //
-// MFMA k mapping. k lane-group g (= lane / MF) takes channels i*KSTEP + g,
-// so for a fixed tap a step advances every operand address by a constant:
-// A by KSTEP, B by KSTEP channel planes of the halo. WS reduction groups
-// split the k-steps of each tap; their partial tiles are added in group order
-// through LDS. STAGES = 2 double-buffers the LDS chunk and keeps the next
-// chunk's loads in flight during the MFMAs. SPLIT > 1 spreads contiguous chunk
-// ranges over grid.z; a second kernel adds the partials in split order.
+// MFMA k mapping. Lane group g (= lane / MF) takes channels i*KSTEP + g, so
+// for a fixed tap a k-step advances the A address by KSTEP*R*S words and the
+// B address by KSTEP channel planes. WS reduction groups split the k-steps of
+// each tap; their partial tiles are added in group order through LDS.
+// STAGES = 2 double-buffers the chunk: the copy of chunk c+1 is in flight
+// while the MFMAs of chunk c run. SPLIT > 1 spreads contiguous chunk ranges
+// over grid.z; a second kernel adds the partials in split order.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -36,7 +38,8 @@
 
 namespace ct {
 
-constexpr int kF32Slots = 16;  // staged elements per thread per chunk: halo + filter (max)
+constexpr int kHaloSlots = 16;  // halo loads per wave per chunk (max)
+constexpr int kFiltSlots = 16;  // filter loads per wave per chunk (max)
 
 struct IgF32Args {
   int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
@@ -46,11 +49,14 @@ struct IgF32Args {
   int ht, wt, lda;
   int bm, bn, threads;
   int cps, chunks;
-  int n_halo, n_filt;  // staged halo / filter elements per thread per chunk
+  int xs_pad;          // halo words per stage: whole wave loads
+  int n_halo;          // halo loads per wave per chunk
+  int n_filt_units;    // filter loads per chunk (all waves): rows x segments
+  int f_nseg;          // 64-word segments per filter row
   // host-precomputed: exact reciprocals for small quotients, and the block
-  // size decomposed over the halo (c, hh, ww) and filter (m, c, tap) indices
-  float inv_plane, inv_wt, inv_perm, inv_rs, inv_tpw;
-  int h_dc, h_dhh, h_dww, f_dm, f_dc, f_dtap;
+  // size decomposed over the halo indices (c, hh, ww)
+  float inv_plane, inv_wt, inv_tpw;
+  int h_dc, h_dhh, h_dww;
   int64_t ny;
 };
 
@@ -86,9 +92,14 @@ constexpr int kOob = 0x7FFFFFF0;  // byte offset beyond every buffer: reads as 0
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
-__device__ __forceinline__ float bload(__amdgpu_buffer_rsrc_t r, int off) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+// One wave instruction: lane i copies the word at byte offset off of r to lds[i].
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 4, off, 0, 0, 0);
 }
+// Waits for this wave's copies to land in LDS.
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 template <int MF, int TM, int TN, int STAGES, int SPEC>
 __global__ void __launch_bounds__(mfma_max_threads(TM * TN * MfmaF32<MF>::ACC))
@@ -108,10 +119,11 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   extern __shared__ float smem[];
   const int cpcp = a.cpcp, bm = a.bm, ht = a.ht, wt = a.wt, lda = a.lda;
   const int plane = ht * wt;
-  const int xs_floats = cpcp * plane;
-  const int stage_floats = xs_floats + bm * lda;
+  const int jw = cpcp * RS;  // filter words per output channel in a chunk
+  const int stage_floats = a.xs_pad + bm * lda;
 
   const int t = threadIdx.x, lane = t & 63, wave = wave_id();
+  const int nw = a.threads >> 6;
   const int wpg = a.wm * a.wn;
   const int wg = wave / wpg, wi = wave - wg * wpg;
   const int wmi = wi / a.wn, wni = wi - wmi * a.wn;
@@ -125,82 +137,74 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int oh0 = th * a.tph, ow0 = tw * a.tpw;
   const int ih0 = oh0 * sh - ph, iw0 = ow0 * sw - pw;
   const int k0 = blockIdx.y * bm, sp = blockIdx.z;
+  const int cl = min(a.cpc, a.C);  // channels of x in a chunk
 
-  // ---- staging plan, fixed for the whole reduction (carry counters) ----
-  // Each thread stages kF32Slots elements per chunk: slots [0, n_halo) are
-  // halo elements, the next n_filt are filter elements, the rest are unused.
-  // Every slot issues its load (an unused or padding slot reads out of range,
-  // i.e. 0) and stores to LDS (an unused slot into a per-lane dummy word), so
-  // the staging code has no branches and all loads are in flight at once.
-  const int dummy = STAGES * stage_floats + lane;
-  // channels of x per chunk: CPC divides C, or one chunk holds all C (< CPC)
-  const int cl = min(a.cpc, a.C);
-  int s_off[kF32Slots], s_lds[kF32Slots];
+  // ---- halo plan: slot i of this wave copies halo words (i*nw + wave)*64 + lane ----
+  int h_off[kHaloSlots];
   {
-    // halo element e = t + i*threads of Xs[cpcp][ht][wt] -> (c, hh, ww)
-    const int T = a.threads;
     int c = qdiv(t, a.inv_plane), rem = t - c * plane;
     int hh = qdiv(rem, a.inv_wt), ww = rem - hh * wt;
-    const int dc = a.h_dc, dhh = a.h_dhh, dww = a.h_dww;
 #pragma unroll
-    for (int i = 0; i < kF32Slots; ++i) {
+    for (int i = 0; i < kHaloSlots; ++i) {
       if (i < a.n_halo) {
         const int gh = ih0 + hh, gw = iw0 + ww;
-        const int e = t + i * T;
-        const bool ok = c < cl && gh >= 0 && gh < a.H && gw >= 0 && gw < a.W;
-        s_off[i] = ok ? ((nimg * a.C + c) * HW + gh * a.W + gw) * 4 : kOob;
-        s_lds[i] = e < xs_floats ? e : -1;
-        ww += dww;
-        if (ww >= wt) { ww -= wt; ++hh; }
-        hh += dhh;
-        if (hh >= ht) { hh -= ht; ++c; }
-        c += dc;
+        const bool ok = c < cl && (unsigned)gh < (unsigned)a.H && (unsigned)gw < (unsigned)a.W;
+        h_off[i] = ok ? (c * HW + gh * a.W + gw) * 4 : kOob;
+        // advance by T words: (c, hh, ww) += (h_dc, h_dhh, h_dww) with carries
+        ww += a.h_dww;
+        const int cw = ww >= wt;
+        ww -= cw ? wt : 0;
+        hh += a.h_dhh + cw;
+        const int chh = hh >= ht;
+        hh -= chh ? ht : 0;
+        c += a.h_dc + chh;
       }
     }
   }
+  // ---- filter plan: slot j of this wave copies 64 words of row m starting at
+  // word f_dst - m*lda, where unit u = j*nw + wave enumerates (m, segment)
+  // row-major. A row shorter than 64 words has a pitch of 65 (the copy's tail
+  // lands in the row's padding); a longer row's last segment is aligned to the
+  // row end, overlapping the one before it with the same data. ----
+  const int nseg = a.f_nseg;
+  const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) / nw : 0;
+  int f_off[kFiltSlots], f_dst[kFiltSlots];
   {
-    // filter element e = t + j*threads of the chunk's BM x CPCP x RS slice, in
-    // global order (m, c, tap); LDS position m*lda + tap*cpcp + c
-    const int per_m = cpcp * RS;
-    int m = qdiv(t, a.inv_perm), rem = t - m * per_m;
-    int c = qdiv(rem, a.inv_rs), tap = rem - c * RS;
-    const int dm = a.f_dm, dcc = a.f_dc, dtap = a.f_dtap;
+    const int dm = nw / nseg, dseg = nw - dm * nseg;
+    int m = wave / nseg, seg = wave - (wave / nseg) * nseg;
 #pragma unroll
-    for (int i = 0; i < kF32Slots; ++i) {
-      const int j = i - a.n_halo;
-      if (j >= 0 && j < a.n_filt) {
-        const bool in_tile = m < bm;
-        const bool ok = in_tile && k0 + m < a.K && c < cl;
-        s_off[i] = ok ? ((k0 + m) * a.kred + c * RS + tap) * 4 : kOob;
-        s_lds[i] = in_tile ? xs_floats + m * lda + tap * cpcp + c : -1;
-        tap += dtap;
-        if (tap >= RS) { tap -= RS; ++c; }
-        c += dcc;
-        if (c >= cpcp) { c -= cpcp; ++m; }
+    for (int j = 0; j < kFiltSlots; ++j) {
+      if (j < n_filt_w) {
+        const int s0 = jw >= 64 ? min(seg * 64, jw - 64) : 0;
+        const int jj = s0 + lane;
+        f_off[j] = jj < cl * RS ? (m * a.kred + jj) * 4 : kOob;
+        f_dst[j] = m * lda + s0;
+        seg += dseg;
         m += dm;
-      } else if (j >= a.n_filt) {
-        s_off[i] = kOob;
-        s_lds[i] = -1;
+        if (seg >= nseg) { seg -= nseg; ++m; }
       }
     }
   }
+
   const int ch_begin = sp * a.cps;
   const int ch_end = min(a.chunks, ch_begin + a.cps);
-  const int64_t xbytes = (int64_t)a.N * a.C * HW * 4, wbytes = (int64_t)a.K * a.kred * 4;
 
-  float rv[kF32Slots];
-  auto load_chunk = [&](int ch) {
+  // start the copies of chunk ch into LDS stage `stage`
+  auto issue = [&](int ch, int stage) {
     const int c0 = ch * a.cpc;
-    // descriptors start at the chunk's first channel
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)c0 * HW, xbytes - (int64_t)c0 * HW * 4);
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)c0 * RS, wbytes - (int64_t)c0 * RS * 4);
+    float* xs = smem + stage * stage_floats;
+    float* as = xs + a.xs_pad;
+    // x: this image's channels [c0, c0 + cl); w: rows [k0, K) from column c0*RS
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(x + ((int64_t)nimg * a.C + c0) * HW, (int64_t)cl * HW * 4);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)k0 * a.kred + (int64_t)c0 * RS,
+                                                ((int64_t)(a.K - k0) * a.kred - (int64_t)c0 * RS) * 4);
 #pragma unroll
-    for (int i = 0; i < kF32Slots; ++i) rv[i] = bload(i < a.n_halo ? rx : rw, s_off[i]);
-  };
-  auto store_chunk = [&](int stage) {
-    const int base = stage * stage_floats;
+    for (int i = 0; i < kHaloSlots; ++i)
+      if (i < a.n_halo) copy_to_lds(rx, xs + (i * nw + wave) * 64, h_off[i]);
 #pragma unroll
-    for (int i = 0; i < kF32Slots; ++i) smem[s_lds[i] >= 0 ? base + s_lds[i] : dummy] = rv[i];
+    for (int j = 0; j < kFiltSlots; ++j)
+      if (j < n_filt_w) copy_to_lds(rw, as + f_dst[j], f_off[j]);
   };
 
   V acc[TM][TN];
@@ -215,7 +219,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int lrow = lane % MF, kg = lane / MF;
   int a_base[TM], b_base[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) a_base[i] = (m_off + i * MF + lrow) * lda + kg;
+  for (int i = 0; i < TM; ++i) a_base[i] = (m_off + i * MF + lrow) * lda + kg * RS;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int q = n_off + j * MF + lrow;
@@ -224,24 +228,25 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   }
   const int n_i = cpcp / KSTEP / a.wsp;  // k-steps per tap for this reduction group
   const int i_begin = wg * n_i;
+  const int astep = KSTEP * RS, bstep = KSTEP * plane;
   // For each tap, the reduction group's channel steps run in groups of 4:
   // all fragment reads of a group are issued before its MFMAs.
   auto compute = [&](int stage) {
     const float* Xs = smem + stage * stage_floats;
-    const float* As = Xs + xs_floats;
+    const float* As = Xs + a.xs_pad;
     for (int r = 0; r < R; ++r) {
       for (int s = 0; s < S; ++s) {
-        const float* ap = As + (r * S + s) * cpcp + i_begin * KSTEP;
-        const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * KSTEP * plane;
+        const float* ap = As + (r * S + s) + i_begin * astep;
+        const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * bstep;
         int ii = 0;
         for (; ii + 4 <= n_i; ii += 4) {
           float fa[4][TM], fb[4][TN];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i) fa[u][i] = ap[a_base[i] + (ii + u) * KSTEP];
+            for (int i = 0; i < TM; ++i) fa[u][i] = ap[a_base[i] + (ii + u) * astep];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) fb[u][j] = bp[b_base[j] + (ii + u) * KSTEP * plane];
+            for (int j = 0; j < TN; ++j) fb[u][j] = bp[b_base[j] + (ii + u) * bstep];
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u)
@@ -253,9 +258,9 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
         for (; ii < n_i; ++ii) {
           float fa[TM], fb[TN];
 #pragma unroll
-          for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * KSTEP];
+          for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * astep];
 #pragma unroll
-          for (int j = 0; j < TN; ++j) fb[j] = bp[b_base[j] + ii * KSTEP * plane];
+          for (int j = 0; j < TN; ++j) fb[j] = bp[b_base[j] + ii * bstep];
 #pragma unroll
           for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -267,25 +272,20 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 
   if constexpr (STAGES == 1) {
     for (int ch = ch_begin; ch < ch_end; ++ch) {
-      load_chunk(ch);
-      __syncthreads();
-      store_chunk(0);
+      issue(ch, 0);
+      wait_copies();
       __syncthreads();
       compute(0);
+      __syncthreads();  // the next chunk's copies overwrite this stage
     }
   } else {
-    if (ch_begin < ch_end) {
-      load_chunk(ch_begin);
-      store_chunk(0);
-      __syncthreads();
-    }
+    if (ch_begin < ch_end) issue(ch_begin, 0);
     for (int ch = ch_begin; ch < ch_end; ++ch) {
       const int cur = (ch - ch_begin) & 1;
-      const bool more = ch + 1 < ch_end;
-      if (more) load_chunk(ch + 1);
+      wait_copies();
+      __syncthreads();  // chunk ch has landed; every wave is done with chunk ch-1
+      if (ch + 1 < ch_end) issue(ch + 1, cur ^ 1);
       compute(cur);
-      if (more) store_chunk(cur ^ 1);
-      __syncthreads();
     }
   }
 

@@ -319,21 +319,30 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const int rs = o.r * o.s;
   const int ht = (tph - 1) * o.stride_h + (o.r - 1) * o.dil_h + 1;
   const int wt = (tpw - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1;
-  const int lda = rs * cpcp + 1;
+  // LDS copies move 64 words per wave instruction: the halo as a flat array
+  // padded to whole loads of every wave, the filter row by row in 64-word
+  // segments; filter rows get an odd pitch of at least 65 words
+  const int nw = threads / 64;
   const int64_t xs = (int64_t)cpcp * ht * wt;
-  g->a_loads = (int)cdiv(xs, threads);                       // halo elements per thread
-  g->b_loads = (int)cdiv((int64_t)bm * cpcp * rs, threads);  // filter elements per thread
-  if (g->a_loads + g->b_loads > 16) REJECT("too many staged loads per thread");
+  const int jw = rs * cpcp;
+  const int nseg = (int)cdiv(jw, 64);
+  const int lda = jw >= 64 ? (jw | 1) : 65;
+  g->a_loads = (int)cdiv(xs, 64 * nw);           // halo loads per wave per chunk
+  g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);  // filter loads per wave per chunk
+  if (g->a_loads > 16) REJECT("too many halo loads per wave");
+  if (g->b_loads > 16) REJECT("too many filter loads per wave");
+  const int64_t xs_pad = (int64_t)g->a_loads * 64 * nw;
   if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
     REJECT("tensor too large for 32-bit buffer offsets");
   const int64_t chunks = cdiv(x.cg, cpc);
   int64_t cps = 0;
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty reduction range");
-  const int64_t stage_bytes = 4 * (xs + (int64_t)bm * lda);
+  const int64_t stage_bytes = 4 * (xs_pad + (int64_t)bm * lda);
   const int64_t red_bytes = wsplit > 1 ? 4 * (int64_t)(wsplit - 1) * bm * bn : 0;
-  // + one word per lane where unused staging slots land
-  const int64_t lbytes = std::max(stages * stage_bytes + 256, red_bytes);
+  const int64_t lbytes = std::max(stages * stage_bytes, red_bytes);
   if (lbytes > kMaxLdsBytes) REJECT("LDS tile too large");
+  g->xs_pad = (int)xs_pad;
+  g->f_nseg = nseg;
   g->bm = bm;
   g->bn = bn;
   g->cpcp = cpcp;
