@@ -243,7 +243,9 @@ typedef struct ct_client {
 } ct_client;
 
 /* Run n_clients clients concurrently, one host thread each, and wait for all.
- * Clients with overlapping masks are allowed but then share CUs. */
+ * Clients with overlapping masks are allowed but then share CUs. With the
+ * environment variable CT_PROGRESS set, each client writes one line to stderr
+ * per finished job. */
 int ct_tune_clients(ct_client *clients, int n_clients, const ct_measure_opts *stage1,
                     const ct_measure_opts *stage2, float eps);
 

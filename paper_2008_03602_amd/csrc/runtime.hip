@@ -2,6 +2,8 @@
 // the timing protocol (profile stage of the tuning loop), tuning clients on
 // disjoint CU masks, cross-evaluation and the probes.
 #include <hip/hip_runtime.h>
+#include <cstdio>
+#include <cstdlib>
 #include <pthread.h>
 #include <sched.h>
 
@@ -386,9 +388,14 @@ static void run_client(ct_client* cl, const ct_measure_opts* o1, const ct_measur
     int rc = make_key(cl->cu_mask, CT_MASK_WORDS, &key);
     StreamCtx* c = nullptr;
     if (!rc) rc = get_ctx(key, &c);
+    // CT_PROGRESS set in the environment: one line on stderr per finished job
+    const bool progress = getenv("CT_PROGRESS") != nullptr;
     for (int i = 0; !rc && i < cl->n_jobs; ++i) {
       rc = tune_job(&cl->jobs[i], c, *o1, *o2, eps);
       if (!rc) cl->n_measured += cl->jobs[i].n_cands;
+      if (progress)
+        fprintf(stderr, "[ct] client on core %d: job %d/%d done, rc %d, %.1f s\n", cl->host_core, i + 1,
+                cl->n_jobs, rc, now_s() - cl->t_start_s);
     }
     cl->rc = rc;
   } catch (...) {

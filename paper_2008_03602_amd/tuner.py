@@ -209,6 +209,17 @@ def fraction_report(results: Sequence[JobResult]) -> dict:
             "clients": len({r.client for r in results})}
 
 
+def cross_eval_regret(matrices: Dict[str, list], fractions: Sequence[float]) -> List[List[float]]:
+    """Mean over layers of M[f][g] / min_f' M[f'][g]: how much slower the
+    schedule tuned at share f runs at share g than the best of the winners."""
+    n = len(fractions)
+    acc = np.zeros((n, n))
+    for M in matrices.values():
+        M = np.asarray(M, dtype=np.float64)
+        acc += M / M.min(axis=0, keepdims=True)
+    return (acc / max(len(matrices), 1)).tolist()
+
+
 def find_layer(name: str):
     """(op, config, layer position) of a named layer of configurations 1-5."""
     for cid in range(1, 6):
@@ -254,6 +265,8 @@ def main(argv=None) -> int:
     ap.add_argument("--clients", type=int, default=None)
     ap.add_argument("--layers", type=int, default=None, help="only the first N layers")
     ap.add_argument("--candidates", type=int, default=None)
+    ap.add_argument("--fractions", default=None, help="comma-separated CU shares (default: the config's)")
+    ap.add_argument("--no-cross-eval", action="store_true", help="skip the cross-evaluation")
     ap.add_argument("--replay", default=None, metavar="LAYER:FAMILY:K0,K1,...",
                     help="run one schedule of one layer and print its latency")
     ap.add_argument("--fraction", type=float, default=1.0, help="CU share for --replay")
@@ -271,6 +284,8 @@ def main(argv=None) -> int:
     cfg = W.config(a.config)
     if a.candidates:
         cfg.n_candidates = a.candidates
+    if a.fractions:
+        cfg.fractions = tuple(float(f) for f in a.fractions.split(","))
     ops = cfg.ops[:a.layers] if a.layers else cfg.ops
     L.ct_init(0)
     layers = [make_layer(op, cfg, i) for i, op in enumerate(ops)]
@@ -284,7 +299,12 @@ def main(argv=None) -> int:
         for r in res:
             winners.setdefault(r.layer_id, {})[f] = r.winner
         print("fraction %.3f: %s" % (f, json.dumps(report["fractions"][str(f)]["throughput"])), flush=True)
-    if len(cfg.fractions) > 1:
+    thr = {f: report["fractions"][str(f)]["throughput"]["candidates_per_s"] for f in cfg.fractions}
+    if 1.0 in thr and len(thr) > 1:
+        report["throughput_vs_one_full_gpu_client"] = {str(f): thr[f] / thr[1.0] for f in cfg.fractions}
+        print("candidates/s relative to one full-GPU client:",
+              json.dumps(report["throughput_vs_one_full_gpu_client"]), flush=True)
+    if len(cfg.fractions) > 1 and not a.no_cross_eval:
         masks = [L.ct_cu_mask(f, 0) for f in cfg.fractions]
         report["cross_eval"] = {}
         for ld in layers:
@@ -293,6 +313,12 @@ def main(argv=None) -> int:
                 continue
             M = cross_eval(ld, ws, masks, cfg.stage2)
             report["cross_eval"][ld.op.name] = M.tolist()
+            print("cross-eval %s done" % ld.op.name, flush=True)
+        report["cross_eval_regret"] = cross_eval_regret(report["cross_eval"], cfg.fractions)
+        print("cross-eval regret (rows: tuned at, columns: run at; mean over layers of "
+              "latency / best latency in the column):", flush=True)
+        for f, row in zip(cfg.fractions, report["cross_eval_regret"]):
+            print("  %5.3f: %s" % (f, " ".join("%6.3f" % v for v in row)), flush=True)
     if a.out:
         with open(a.out, "w") as fh:
             json.dump(report, fh, indent=1)
