@@ -2,7 +2,8 @@
 batch-1 conv set (12 layers, fp32 NCHW, 256 seeded candidates per layer):
 
   1. tune every layer at 25% of the CUs, as 4 concurrent clients on the 4
-     disjoint 64-CU slots (layers dealt round-robin, 3 per client);
+     disjoint 64-CU slots, which take the layers from one shared queue,
+     largest first;
   2. the same at 50% (2 clients on 128-CU slots) and at 100% (1 client);
      each client screens every candidate (2 warm-up + 5 x 10 timed runs),
      re-measures its top 8 (21 x 10 runs, interleaved) and picks the winner;
@@ -44,7 +45,7 @@ def runs_per_candidate(cfg, n_layers: int, n_fractions: int) -> float:
     return runs / (n_layers * n_fractions * cfg.n_candidates)
 
 
-def cpu_baseline(cfg, runs_per_cand: float, budget_s: float = 20.0) -> dict:
+def cpu_baseline(cfg, runs_per_cand: float, budget_s: float = 15.0) -> dict:
     """The fp64 oracle timed on this host on a bounded sample of the workload.
 
     One oracle convolution stands in for one convolution launch of the tuner, so
@@ -55,7 +56,7 @@ def cpu_baseline(cfg, runs_per_cand: float, budget_s: float = 20.0) -> dict:
     threads = len(os.sched_getaffinity(0))
     done, flops, t_total = 0, 0, 0.0
     # the layer list is walked round-robin until the time budget is used
-    while t_total < budget_s and done < 50 * len(cfg.ops):
+    while t_total < budget_s:
         op = cfg.ops[done % len(cfg.ops)]
         x, w = synth.conv_inputs(op.x_shape(), op.w_shape(), cfg.dist, cfg.seed, cfg.config_id,
                                  done % len(cfg.ops))
@@ -161,8 +162,8 @@ def main() -> int:
         "ms_per_step": elapsed / a.steps * 1e3, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": "ResNet-18 b1 conv set (12 layers) fp32 NCHW, %d seeded candidates per layer, "
-                               "tuned at 25/50/100%% CUs by 4/2/1 concurrent CU-masked clients, then a 3x3 "
-                               "cross-evaluation of the winners" % cfg.n_candidates,
+                               "tuned at 25/50/100%% CUs by 4/2/1 concurrent CU-masked clients sharing a "
+                               "largest-first layer queue, then a 3x3 cross-evaluation of the winners" % cfg.n_candidates,
                    "candidates_per_step": n_per_step, "layers": len(layers), "seed": cfg.seed,
                    "protocol": {"screen": [cfg.stage1.warmup, cfg.stage1.repeats, cfg.stage1.launches],
                                 "remeasure_top": cfg.top_t,

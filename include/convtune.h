@@ -249,6 +249,17 @@ typedef struct ct_client {
 int ct_tune_clients(ct_client *clients, int n_clients, const ct_measure_opts *stage1,
                     const ct_measure_opts *stage2, float eps);
 
+/* The same clients fed from one queue: the jobs are taken in array order, each
+ * by whichever client is idle first, so a model's layers spread over the
+ * clients by their actual cost (list them longest first for the shortest
+ * makespan). The clients' jobs / n_jobs fields are ignored; their other
+ * fields are used as above. job_client (out, may be NULL) receives, per job,
+ * the index of the client that ran it (-1 if none did). Returns 0, or the
+ * code of the first client that failed (the other clients keep taking jobs). */
+int ct_tune_shared(ct_client *clients, int n_clients, ct_tune_job *jobs, int n_jobs,
+                   const ct_measure_opts *stage1, const ct_measure_opts *stage2, float eps,
+                   int32_t *job_client);
+
 /* ---- cross-evaluation (section 2.2.1, Tables 1-2: tuned at f, run at g) ---- */
 
 /* M[i * n_masks + j] = stage-2 latency of schedule s[i] run on mask j. The

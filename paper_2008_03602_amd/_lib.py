@@ -92,6 +92,8 @@ _SIGS = {
     "ct_top_t": (c_i32, [P(c_f32), P(c_i32), c_i32, c_i32, P(c_i32), P(c_i32)]),
     "ct_select_winner": (c_i32, [P(c_f32), P(c_i32), c_i32, c_f32, P(c_i32)]),
     "ct_tune_clients": (c_i32, [P(ct_client), c_i32, P(ct_measure_opts), P(ct_measure_opts), c_f32]),
+    "ct_tune_shared": (c_i32, [P(ct_client), c_i32, P(ct_tune_job), c_i32, P(ct_measure_opts),
+                               P(ct_measure_opts), c_f32, P(c_i32)]),
     "ct_cross_eval": (c_i32, [P(ct_op), P(ct_schedule), c_i32, P(c_u32), c_i32, c_i32, P(ct_measure_opts),
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, P(c_f32)]),
     "ct_probe_cus": (c_i32, [P(c_u32), c_i32, c_i32, P(c_i32), c_i32, P(c_i32)]),
@@ -331,6 +333,15 @@ def ct_select_winner(lat: np.ndarray, pos: np.ndarray, eps: float) -> int:
 
 def ct_tune_clients(clients: ctypes.Array, opts1: ct_measure_opts, opts2: ct_measure_opts, eps: float) -> None:
     _check(lib().ct_tune_clients(clients, len(clients), ctypes.byref(opts1), ctypes.byref(opts2), eps))
+
+
+def ct_tune_shared(clients: ctypes.Array, jobs: ctypes.Array, opts1: ct_measure_opts, opts2: ct_measure_opts,
+                   eps: float) -> np.ndarray:
+    """Run the clients on one shared job queue; returns the client index per job."""
+    owner = np.full(max(len(jobs), 1), -1, dtype=np.int32)
+    _check(lib().ct_tune_shared(clients, len(clients), jobs, len(jobs), ctypes.byref(opts1), ctypes.byref(opts2),
+                                eps, _arr(owner, c_i32)))
+    return owner[:len(jobs)]
 
 
 def ct_cross_eval(op, scheds: Sequence, masks: Sequence, opts: ct_measure_opts, x, w, y) -> np.ndarray:

@@ -377,7 +377,17 @@ static int tune_job(ct_tune_job* j, StreamCtx* c, const ct_measure_opts& o1, con
   return CT_OK;
 }
 
-static void run_client(ct_client* cl, const ct_measure_opts* o1, const ct_measure_opts* o2, float eps) {
+// The jobs a client runs: its own list in order, or (next != nullptr) the
+// next unclaimed job of a queue shared by all clients.
+struct JobSource {
+  ct_tune_job* jobs;
+  int n;
+  std::atomic<int>* next;
+  int32_t* owner;  // shared queue: owner[i] = index of the client that ran job i
+};
+
+static void run_client(ct_client* cl, int index, JobSource src, const ct_measure_opts* o1,
+                       const ct_measure_opts* o2, float eps) {
   pin_to_core(cl->host_core);
   cl->rc = CT_OK;
   cl->n_measured = 0;
@@ -390,12 +400,16 @@ static void run_client(ct_client* cl, const ct_measure_opts* o1, const ct_measur
     if (!rc) rc = get_ctx(key, &c);
     // CT_PROGRESS set in the environment: one line on stderr per finished job
     const bool progress = getenv("CT_PROGRESS") != nullptr;
-    for (int i = 0; !rc && i < cl->n_jobs; ++i) {
-      rc = tune_job(&cl->jobs[i], c, *o1, *o2, eps);
-      if (!rc) cl->n_measured += cl->jobs[i].n_cands;
+    for (int k = 0; !rc; ++k) {
+      int i = k;
+      if (src.next) i = src.next->fetch_add(1);
+      if (i >= src.n) break;
+      if (src.owner) src.owner[i] = index;
+      rc = tune_job(&src.jobs[i], c, *o1, *o2, eps);
+      if (!rc) cl->n_measured += src.jobs[i].n_cands;
       if (progress)
-        fprintf(stderr, "[ct] client on core %d: job %d/%d done, rc %d, %.1f s\n", cl->host_core, i + 1,
-                cl->n_jobs, rc, now_s() - cl->t_start_s);
+        fprintf(stderr, "[ct] client %d: job %d of %d done, rc %d, %.1f s\n", index, i + 1, src.n, rc,
+                now_s() - cl->t_start_s);
     }
     cl->rc = rc;
   } catch (...) {
@@ -403,6 +417,20 @@ static void run_client(ct_client* cl, const ct_measure_opts* o1, const ct_measur
     cl->rc = CT_E_ARG;
   }
   cl->t_end_s = now_s();
+}
+
+static int run_clients(ct_client* clients, int n_clients, const std::vector<JobSource>& src,
+                       const ct_measure_opts* stage1, const ct_measure_opts* stage2, float eps) {
+  std::vector<std::thread> th;
+  th.reserve(n_clients);
+  for (int i = 0; i < n_clients; ++i) th.emplace_back(run_client, &clients[i], i, src[i], stage1, stage2, eps);
+  for (auto& t : th) t.join();
+  for (int i = 0; i < n_clients; ++i)
+    if (clients[i].rc) {
+      set_error("tuning client " + std::to_string(i) + " failed with code " + std::to_string(clients[i].rc));
+      return clients[i].rc;
+    }
+  return CT_OK;
 }
 
 }  // namespace ct
@@ -528,16 +556,26 @@ int ct_tune_clients(ct_client* clients, int n_clients, const ct_measure_opts* st
     set_error("ct_tune_clients: bad argument");
     return CT_E_ARG;
   }
-  std::vector<std::thread> th;
-  th.reserve(n_clients);
-  for (int i = 0; i < n_clients; ++i) th.emplace_back(run_client, &clients[i], stage1, stage2, eps);
-  for (auto& t : th) t.join();
-  for (int i = 0; i < n_clients; ++i)
-    if (clients[i].rc) {
-      set_error("tuning client " + std::to_string(i) + " failed with code " + std::to_string(clients[i].rc));
-      return clients[i].rc;
-    }
-  return CT_OK;
+  std::vector<JobSource> src(n_clients);
+  for (int i = 0; i < n_clients; ++i) src[i] = {clients[i].jobs, clients[i].n_jobs, nullptr, nullptr};
+  return run_clients(clients, n_clients, src, stage1, stage2, eps);
+}
+
+int ct_tune_shared(ct_client* clients, int n_clients, ct_tune_job* jobs, int n_jobs,
+                   const ct_measure_opts* stage1, const ct_measure_opts* stage2, float eps,
+                   int32_t* job_client) {
+  int rc = check_init();
+  if (rc) return rc;
+  if (!clients || n_clients < 1 || n_clients > 64 || n_jobs < 0 || (n_jobs > 0 && !jobs) || !opts_ok(stage1) ||
+      !opts_ok(stage2) || !(eps >= 0.f)) {
+    set_error("ct_tune_shared: bad argument");
+    return CT_E_ARG;
+  }
+  if (job_client)
+    for (int i = 0; i < n_jobs; ++i) job_client[i] = -1;
+  std::atomic<int> next{0};
+  std::vector<JobSource> src(n_clients, JobSource{jobs, n_jobs, &next, job_client});
+  return run_clients(clients, n_clients, src, stage1, stage2, eps);
 }
 
 int ct_cross_eval(const ct_op* op, const ct_schedule* s, int n_sched, const uint32_t* masks, int n_masks,

@@ -8,8 +8,8 @@ build, profile on the device, pick the best. Its scaling (section 3.1.1):
 several profiling servers with fixed GPU shares, and a model's operators
 sharded over several tuning clients whose results are merged. Here a client
 is a library thread with its own CU-masked stream; the operators of a model
-are dealt to the clients round-robin, and the merged result is the per-layer
-winner. Cross-evaluation (section 2.2.1, Tables 1-2) re-runs the schedule
+are taken by the clients from one shared queue, largest first (or dealt
+round-robin), and the merged result is the per-layer winner. Cross-evaluation (section 2.2.1, Tables 1-2) re-runs the schedule
 tuned at one share on every other share.
 """
 from __future__ import annotations
@@ -114,6 +114,44 @@ class _Keep:
         return x
 
 
+def _fill_job(jb, ld: LayerData, c: List[L.ct_schedule], cfg: W.TuneConfig, keep: _Keep,
+              verify_refs: Optional[Dict[int, torch.Tensor]], verify_tol: float):
+    """Point one ct_tune_job at a layer's buffers, candidates and result arrays."""
+    arr = keep.add(L.schedule_array(c))
+    n = len(c)
+    lat1 = keep.add(np.zeros(max(n, 1), np.float32))
+    st1 = keep.add(np.zeros(max(n, 1), np.int32))
+    top = keep.add(np.zeros(cfg.top_t, np.int32))
+    lat2 = keep.add(np.zeros(cfg.top_t, np.float32))
+    jb.op = L.make_op(ld.op)
+    jb.x, jb.w, jb.y = ld.x.data_ptr(), ld.w.data_ptr(), ld.y.data_ptr()
+    jb.cands, jb.n_cands = arr, n
+    if verify_refs is not None and ld.layer_id in verify_refs:
+        jb.verify = L.ct_verify(verify_refs[ld.layer_id].data_ptr(), verify_tol)
+    jb.lat1_us = lat1.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    jb.status1 = st1.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    jb.top_t = cfg.top_t
+    jb.top_pos = top.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    jb.lat2_us = lat2.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    return (ld, c, lat1, st1, top, lat2)
+
+
+def _result(jb, meta, client: int, fraction: float) -> JobResult:
+    ld, c, lat1, st1, top, lat2 = meta
+    n, nt = len(c), jb.n_top
+    return JobResult(ld.op, ld.layer_id, client, fraction, list(c), lat1[:n].copy(), st1[:n].copy(),
+                     top[:nt].copy(), lat2[:nt].copy(), jb.winner_pos, jb.winner_lat_us, jb.t_start_s, jb.t_end_s)
+
+
+def _clients(masks: Sequence[np.ndarray], pin_cores: bool) -> ctypes.Array:
+    clients = (L.ct_client * len(masks))()
+    for j, m in enumerate(masks):
+        for k, v in enumerate(m):
+            clients[j].cu_mask[k] = int(v)
+        clients[j].host_core = j if pin_cores else -1
+    return clients
+
+
 def tune_clients(assignments: Sequence[Sequence[LayerData]], masks: Sequence[np.ndarray],
                  cands: Dict[int, List[L.ct_schedule]], cfg: W.TuneConfig, fraction: float,
                  verify_refs: Optional[Dict[int, torch.Tensor]] = None, verify_tol: float = 1e-4,
@@ -124,48 +162,44 @@ def tune_clients(assignments: Sequence[Sequence[LayerData]], masks: Sequence[np.
     layer's candidate list (sample order). Returns one JobResult per layer.
     """
     keep = _Keep()
-    clients = (L.ct_client * len(assignments))()
+    clients = _clients(masks, pin_cores)
     jobs_meta = []
     for j, layers in enumerate(assignments):
         jobs = keep.add((L.ct_tune_job * max(len(layers), 1))())
         for i, ld in enumerate(layers):
-            c = cands[ld.layer_id]
-            arr = keep.add(L.schedule_array(c))
-            n = len(c)
-            lat1 = keep.add(np.zeros(max(n, 1), np.float32))
-            st1 = keep.add(np.zeros(max(n, 1), np.int32))
-            top = keep.add(np.zeros(cfg.top_t, np.int32))
-            lat2 = keep.add(np.zeros(cfg.top_t, np.float32))
-            jb = jobs[i]
-            jb.op = L.make_op(ld.op)
-            jb.x, jb.w, jb.y = ld.x.data_ptr(), ld.w.data_ptr(), ld.y.data_ptr()
-            jb.cands, jb.n_cands = arr, n
-            if verify_refs is not None and ld.layer_id in verify_refs:
-                jb.verify = L.ct_verify(verify_refs[ld.layer_id].data_ptr(), verify_tol)
-            jb.lat1_us = lat1.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
-            jb.status1 = st1.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
-            jb.top_t = cfg.top_t
-            jb.top_pos = top.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
-            jb.lat2_us = lat2.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
-            jobs_meta.append((j, i, ld, c, lat1, st1, top, lat2))
-        cl = clients[j]
-        for k, v in enumerate(masks[j]):
-            cl.cu_mask[k] = int(v)
-        cl.host_core = j if pin_cores else -1
-        cl.jobs = ctypes.cast(jobs, ctypes.POINTER(L.ct_tune_job))
-        cl.n_jobs = len(layers)
-        keep.add(jobs)
+            jobs_meta.append((j, i, _fill_job(jobs[i], ld, cands[ld.layer_id], cfg, keep, verify_refs, verify_tol)))
+        clients[j].jobs = ctypes.cast(jobs, ctypes.POINTER(L.ct_tune_job))
+        clients[j].n_jobs = len(layers)
     o1 = L.opts_from_protocol(cfg.stage1, batch=batch)
     o2 = L.opts_from_protocol(cfg.stage2, batch=cfg.top_t, interleave=1)
     L.ct_tune_clients(clients, o1, o2, cfg.eps)
     out = []
-    for (j, i, ld, c, lat1, st1, top, lat2) in jobs_meta:
+    for (j, i, meta) in jobs_meta:
         jb = ctypes.cast(clients[j].jobs, ctypes.POINTER(L.ct_tune_job))[i]
-        n, nt = len(c), jb.n_top
-        out.append(JobResult(ld.op, ld.layer_id, j, fraction, list(c), lat1[:n].copy(), st1[:n].copy(),
-                             top[:nt].copy(), lat2[:nt].copy(), jb.winner_pos, jb.winner_lat_us,
-                             jb.t_start_s, jb.t_end_s))
+        out.append(_result(jb, meta, j, fraction))
     return out
+
+
+def tune_shared(layers: Sequence[LayerData], masks: Sequence[np.ndarray], cands: Dict[int, List[L.ct_schedule]],
+                cfg: W.TuneConfig, fraction: float, verify_refs: Optional[Dict[int, torch.Tensor]] = None,
+                verify_tol: float = 1e-4, pin_cores: bool = True, batch: int = 16) -> List[JobResult]:
+    """Run one client per mask on a shared queue of layers, taken in the given
+    order by whichever client is idle first. Returns one JobResult per layer."""
+    keep = _Keep()
+    clients = _clients(masks, pin_cores)
+    jobs = (L.ct_tune_job * max(len(layers), 1))()
+    metas = [_fill_job(jobs[i], ld, cands[ld.layer_id], cfg, keep, verify_refs, verify_tol)
+             for i, ld in enumerate(layers)]
+    o1 = L.opts_from_protocol(cfg.stage1, batch=batch)
+    o2 = L.opts_from_protocol(cfg.stage2, batch=cfg.top_t, interleave=1)
+    owner = L.ct_tune_shared(clients, (L.ct_tune_job * len(layers)).from_address(ctypes.addressof(jobs)),
+                             o1, o2, cfg.eps)
+    return [_result(jobs[i], metas[i], int(owner[i]), fraction) for i in range(len(layers))]
+
+
+def largest_first(layers: Sequence[LayerData]) -> List[LayerData]:
+    """Queue order for a shared queue: layers by decreasing FLOPs (ties in table order)."""
+    return sorted(layers, key=lambda ld: (-ld.op.flops(), ld.layer_id))
 
 
 def round_robin(layers: Sequence[LayerData], k: int) -> List[List[LayerData]]:
@@ -192,12 +226,20 @@ def sample_all(layers: Sequence[LayerData], cfg: W.TuneConfig) -> Dict[int, List
 
 
 def tune_model_at_fraction(layers: Sequence[LayerData], cands, cfg: W.TuneConfig, fraction: float,
-                           clients: Optional[int] = None, **kw) -> List[JobResult]:
+                           clients: Optional[int] = None, sharding: str = "queue", **kw) -> List[JobResult]:
     """Tune every layer at CU share `fraction`, with as many concurrent clients as
-    disjoint slots of that share fit on the device (or `clients`)."""
+    disjoint slots of that share fit on the device (or `clients`).
+
+    sharding "queue": the clients take layers from one queue, largest first;
+    "round_robin": layer i goes to client i mod k, in table order."""
     k = clients or max(1, int(round(1.0 / fraction)))
     k = min(k, len(layers))
     masks = [L.ct_cu_mask(fraction, j) for j in range(k)]
+    if sharding == "queue":
+        res = tune_shared(largest_first(layers), masks, cands, cfg, fraction, **kw)
+        return sorted(res, key=lambda r: r.layer_id)
+    if sharding != "round_robin":
+        raise ValueError("sharding is 'queue' or 'round_robin'")
     return tune_clients(round_robin(layers, k), masks, cands, cfg, fraction, **kw)
 
 
@@ -267,6 +309,8 @@ def main(argv=None) -> int:
     ap.add_argument("--candidates", type=int, default=None)
     ap.add_argument("--fractions", default=None, help="comma-separated CU shares (default: the config's)")
     ap.add_argument("--no-cross-eval", action="store_true", help="skip the cross-evaluation")
+    ap.add_argument("--sharding", default="queue", choices=("queue", "round_robin"),
+                    help="how a model's layers are spread over the clients")
     ap.add_argument("--replay", default=None, metavar="LAYER:FAMILY:K0,K1,...",
                     help="run one schedule of one layer and print its latency")
     ap.add_argument("--fraction", type=float, default=1.0, help="CU share for --replay")
@@ -293,7 +337,7 @@ def main(argv=None) -> int:
     report = {"config": cfg.describe(), "fractions": {}}
     winners = {}
     for f in cfg.fractions:
-        res = tune_model_at_fraction(layers, cands, cfg, f, clients=a.clients)
+        res = tune_model_at_fraction(layers, cands, cfg, f, clients=a.clients, sharding=a.sharding)
         report["fractions"][str(f)] = {"throughput": fraction_report(res),
                                        "layers": [r.summary() for r in res]}
         for r in res:

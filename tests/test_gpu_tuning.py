@@ -85,6 +85,24 @@ def test_four_clients_run_concurrently_and_outpace_one():
     assert ratio > 1.3
 
 
+def test_shared_queue_runs_every_layer_once_and_matches_round_robin_lists():
+    cfg = _small_cfg(n_candidates=12, top_t=2)
+    layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops[:6])]
+    cands = T.sample_all(layers, cfg)
+    note("shared queue: 3 clients x 6 layers at 25%")
+    masks = [L.ct_cu_mask(0.25, j) for j in range(3)]
+    res = T.tune_shared(T.largest_first(layers), masks, cands, cfg, 0.25)
+    assert sorted(r.layer_id for r in res) == list(range(6))
+    assert all(0 <= r.client < 3 and r.winner_pos >= 0 for r in res)
+    assert all(np.all(r.status1 == L.S_OK) for r in res)
+    # each client's jobs run one after another
+    for c in range(3):
+        spans = sorted((r.t_start, r.t_end) for r in res if r.client == c)
+        assert all(a[1] <= b[0] + 1e-6 for a, b in zip(spans, spans[1:]))
+    for r in res:
+        assert [L.schedule_tuple(s) for s in r.candidates] == [L.schedule_tuple(s) for s in cands[r.layer_id]]
+
+
 def test_compute_bound_latency_scales_with_cu_share():
     op = W.config(1).ops[0]
     cfg = _small_cfg()
