@@ -33,6 +33,11 @@ int launch_direct_f32(const OpX& x, const ct_schedule& s, const Geom& g, const v
   a.threads = g.threads;
   a.cols = a.tow / s.knob[MW];
   a.tp = a.toh * a.cols;
+  const int rs = o.r * o.s;
+  a.inv_plane = 1.0f / (float)(a.ih_t * a.iw_t);
+  a.inv_iwt = 1.0f / (float)a.iw_t;
+  a.inv_crs = 1.0f / (float)(a.ct * rs);
+  a.inv_rs = 1.0f / (float)rs;
   a.ny = x.ny;
   DirectFn fn = pick_direct(s.knob[MK], s.knob[MW], s.knob[LDS], g.spec, s.knob[UNR]);
   dim3 grid((unsigned)(g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.tiles_n);

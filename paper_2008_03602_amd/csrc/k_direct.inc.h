@@ -30,6 +30,8 @@ struct DirectArgs {
   int split, cps;
   int ih_t, iw_t;
   int threads, tp, cols;
+  // host-precomputed reciprocals of the staging divisors (see qdiv)
+  float inv_plane, inv_iwt, inv_crs, inv_rs;
   int64_t ny;
 };
 
@@ -84,9 +86,9 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int e = e0 + u * a.threads;
-          const int c = e / plane;
+          const int c = qdiv(e, a.inv_plane);
           const int rem = e - c * plane;
-          const int hh = rem / a.iw_t, ww = rem - hh * a.iw_t;
+          const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
           const int gh = ih_org + hh, gw = iw_org + ww;
           const bool ok = e < xt && c < nc && gh >= 0 && gh < H && gw >= 0 && gw < W;
           v[u] = load_or_zero(xn, ((int64_t)(cc + c) * H + gh) * W + gw, ok);
@@ -102,9 +104,9 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int e = e0 + u * a.threads;
-          const int kk = e / crs;
+          const int kk = qdiv(e, a.inv_crs);
           const int rem = e - kk * crs;
-          const int c = rem / RS, rs = rem - c * RS;
+          const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
           const bool ok = e < wt && k0 + kk < K && c < nc;
           v[u] = load_or_zero(w, ((int64_t)(k0 + kk) * C + cc + c) * RS + rs, ok);
         }
@@ -135,32 +137,44 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
       }
       __syncthreads();
     } else {
+      // kb: first output channel of this thread. When every wave lies inside
+      // one channel group (TP a multiple of 64), kb is the same on all lanes
+      // and the filter reads are scalar loads, off the vector memory path.
+      auto direct = [&](const int kb) {
+        // filter rows of this thread's channels; a channel past K reads row
+        // K-1 (its sums are never stored)
+        const float* wrow[MK];
+#pragma unroll
+        for (int i = 0; i < MK; ++i) wrow[i] = w + (int64_t)min(kb + i, K - 1) * C * RS;
 #pragma unroll UNR
-      for (int c = 0; c < nc; ++c) {
-        const float* xc = xn + (int64_t)(cc + c) * H * W;
-        for (int r = 0; r < R; ++r) {
-          const int gh = oh * sh - ph + r * dh;
-          const bool hok = gh >= 0 && gh < H && oh < a.OH;
-          for (int s = 0; s < S; ++s) {
-            float xv[MW], wv[MK];
+        for (int c = 0; c < nc; ++c) {
+          const float* xc = xn + (int64_t)(cc + c) * H * W;
+          const int co = (cc + c) * RS;
+          for (int r = 0; r < R; ++r) {
+            const int gh = oh * sh - ph + r * dh;
+            const bool hok = gh >= 0 && gh < H && oh < a.OH;
+            for (int s = 0; s < S; ++s) {
+              float xv[MW], wv[MK];
 #pragma unroll
-            for (int j = 0; j < MW; ++j) {
-              const int ow = ow0 + lc + j * a.cols;
-              const int gw = ow * sw - pw + s * dw;
-              xv[j] = load_or_zero(xc, (int64_t)gh * W + gw, hok && gw >= 0 && gw < W);
+              for (int j = 0; j < MW; ++j) {
+                const int ow = ow0 + lc + j * a.cols;
+                const int gw = ow * sw - pw + s * dw;
+                xv[j] = load_or_zero(xc, (int64_t)gh * W + gw, hok && gw >= 0 && gw < W);
+              }
+#pragma unroll
+              for (int i = 0; i < MK; ++i) wv[i] = wrow[i][co + r * S + s];
+#pragma unroll
+              for (int i = 0; i < MK; ++i)
+#pragma unroll
+                for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
             }
-#pragma unroll
-            for (int i = 0; i < MK; ++i) {
-              const int k = kbase + i;
-              wv[i] = load_or_zero(w, ((int64_t)k * C + cc + c) * RS + r * S + s, k < K);
-            }
-#pragma unroll
-            for (int i = 0; i < MK; ++i)
-#pragma unroll
-              for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
           }
         }
-      }
+      };
+      if ((a.tp & 63) == 0)
+        direct(__builtin_amdgcn_readfirstlane(kbase));
+      else
+        direct(kbase);
     }
   }
 

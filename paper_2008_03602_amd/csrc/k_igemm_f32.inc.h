@@ -60,10 +60,6 @@ struct IgF32Args {
   int64_t ny;
 };
 
-// floor(n / d) for 0 <= n < 2^22 given inv = 1/d in fp32: (n + 1/2)/d lies at
-// least 1/(2d) from an integer and the fp32 product errs by less than that.
-__device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
-
 __host__ __device__ constexpr int ig_spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
 __host__ __device__ constexpr int ig_spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
 // Threads per block that leave room for the accumulator tile in registers.

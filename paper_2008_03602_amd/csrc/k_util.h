@@ -14,6 +14,10 @@ __device__ __forceinline__ T load_or_zero(const T* __restrict__ p, int64_t idx, 
   return ok ? v : T{};
 }
 
+// floor(n / d) for 0 <= n < 2^22 given inv = 1/d in fp32: (n + 1/2)/d lies at
+// least 1/(2d) from an integer and the fp32 product errs by less than that.
+__device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
+
 // The wave index as a scalar value, so loops bounded by per-wave values stay
 // uniform (scalar branches, unrollable) instead of exec-masked.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
