@@ -37,13 +37,13 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.cps = g.chunks_per_split; a.chunks = g.chunks;
   a.n_halo = g.a_loads; a.n_filt_units = g.bm * g.f_nseg;
   a.xs_pad = g.xs_pad; a.f_nseg = g.f_nseg;
-  const int plane = a.ht * a.wt, T = a.threads;
-  a.inv_plane = 1.0f / (float)plane;
+  const int T = a.threads;
+  a.pp = g.hpp;
+  a.inv_pp = 1.0f / (float)a.pp;
   a.inv_wt = 1.0f / (float)a.wt;
   a.inv_tpw = 1.0f / (float)a.tpw;
-  a.h_dc = T / plane;
-  a.h_dhh = (T % plane) / a.wt;
-  a.h_dww = (T % plane) % a.wt;
+  a.h_dc = T / a.pp;
+  a.h_drem = T % a.pp;
   a.ny = x.ny;
   IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);
   dim3 grid((unsigned)(o.n * g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.split);

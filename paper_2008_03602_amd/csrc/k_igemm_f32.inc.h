@@ -10,11 +10,16 @@
 // Staging. The reduction advances one chunk of CPC input channels at a time
 // (CPC divides C, or a single chunk holds all of C), padded to CPCP channels
 // so that every reduction group gets whole MFMA k-steps. A chunk stages in LDS
-//   * the input halo of the pixel rectangle, Xs[CPCP][HT][WT]: every filter
-//     tap reads its operand from this tile, so a 3x3 filter costs one global
-//     read per input element instead of nine;
-//   * the filter slice As[BM][CPCP*R*S] in global order, rows padded to an odd
-//     pitch LDA so that the rows one MFMA operand reads fall in distinct banks.
+//   * the input halo of the pixel rectangle, Xs[CPCP][HT][WT], each channel
+//     padded to PP words: every filter tap reads its operand from this tile,
+//     so a 3x3 filter costs one global read per input element instead of nine;
+//   * the filter slice As[BM][CPCP*R*S] in global order, rows padded to a
+//     pitch LDA.
+// The pitches keep MFMA operand reads free of bank conflicts (32 banks, half
+// a wave per pass): for 16x16x4 one pass reads 16 rows of A at two k offsets
+// R*S apart (odd) and 16 pixels of B at two channels, so LDA = 2 (mod 32) and
+// PP = 16 (mod 32); for 32x32x2 one pass reads 32 rows of A at one k, so LDA
+// is odd.
 // Both are copied by buffer loads that write LDS directly, without a round
 // trip through registers: one wave instruction fills 64 consecutive LDS
 // words, lane i the i-th. The halo is copied as a flat array; the lanes'
@@ -53,10 +58,11 @@ struct IgF32Args {
   int n_halo;          // halo loads per wave per chunk
   int n_filt_units;    // filter loads per chunk (all waves): rows x segments
   int f_nseg;          // 64-word segments per filter row
+  int pp;              // LDS words per halo channel (the plane plus bank padding)
   // host-precomputed: exact reciprocals for small quotients, and the block
-  // size decomposed over the halo indices (c, hh, ww)
-  float inv_plane, inv_wt, inv_tpw;
-  int h_dc, h_dhh, h_dww;
+  // size decomposed over the halo's (channel, word of the channel)
+  float inv_pp, inv_wt, inv_tpw;
+  int h_dc, h_drem;
   int64_t ny;
 };
 
@@ -114,7 +120,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 
   extern __shared__ float smem[];
   const int cpcp = a.cpcp, bm = a.bm, ht = a.ht, wt = a.wt, lda = a.lda;
-  const int plane = ht * wt;
+  const int plane = ht * wt, pp = a.pp;
   const int jw = cpcp * RS;  // filter words per output channel in a chunk
   const int stage_floats = a.xs_pad + bm * lda;
 
@@ -135,33 +141,31 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int k0 = blockIdx.y * bm, sp = blockIdx.z;
   const int cl = min(a.cpc, a.C);  // channels of x in a chunk
 
-  // ---- halo plan: slot i of this wave copies halo words (i*nw + wave)*64 + lane ----
+  // ---- halo plan: slot i of this wave copies halo words (i*nw + wave)*64 + lane
+  // of Xs[CPCP][PP]; a word of a channel at or past the plane is bank padding ----
   int h_off[kHaloSlots];
   {
-    int c = qdiv(t, a.inv_plane), rem = t - c * plane;
-    int hh = qdiv(rem, a.inv_wt), ww = rem - hh * wt;
+    int c = qdiv(t, a.inv_pp), rem = t - c * pp;
 #pragma unroll
     for (int i = 0; i < kHaloSlots; ++i) {
       if (i < a.n_halo) {
+        const int hh = qdiv(rem, a.inv_wt), ww = rem - hh * wt;
         const int gh = ih0 + hh, gw = iw0 + ww;
-        const bool ok = c < cl && (unsigned)gh < (unsigned)a.H && (unsigned)gw < (unsigned)a.W;
+        const bool ok = c < cl && rem < plane && (unsigned)gh < (unsigned)a.H && (unsigned)gw < (unsigned)a.W;
         h_off[i] = ok ? (c * HW + gh * a.W + gw) * 4 : kOob;
-        // advance by T words: (c, hh, ww) += (h_dc, h_dhh, h_dww) with carries
-        ww += a.h_dww;
-        const int cw = ww >= wt;
-        ww -= cw ? wt : 0;
-        hh += a.h_dhh + cw;
-        const int chh = hh >= ht;
-        hh -= chh ? ht : 0;
-        c += a.h_dc + chh;
+        // advance by T words: (c, rem) += (h_dc, h_drem) with a carry
+        rem += a.h_drem;
+        const int cr = rem >= pp;
+        rem -= cr ? pp : 0;
+        c += a.h_dc + cr;
       }
     }
   }
   // ---- filter plan: slot j of this wave copies 64 words of row m starting at
   // word f_dst - m*lda, where unit u = j*nw + wave enumerates (m, segment)
-  // row-major. A row shorter than 64 words has a pitch of 65 (the copy's tail
-  // lands in the row's padding); a longer row's last segment is aligned to the
-  // row end, overlapping the one before it with the same data. ----
+  // row-major. A row shorter than 64 words has a pitch of at least 64 (the
+  // copy's tail lands in the row's padding); a longer row's last segment is
+  // aligned to the row end, overlapping the one before it with the same data. ----
   const int nseg = a.f_nseg;
   const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) / nw : 0;
   int f_off[kFiltSlots], f_dst[kFiltSlots];
@@ -220,47 +224,63 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   for (int j = 0; j < TN; ++j) {
     const int q = n_off + j * MF + lrow;
     const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
-    b_base[j] = kg * plane + (pr * sh) * wt + pc * sw;
+    b_base[j] = kg * pp + (pr * sh) * wt + pc * sw;
   }
   const int n_i = cpcp / KSTEP / a.wsp;  // k-steps per tap for this reduction group
   const int i_begin = wg * n_i;
-  const int astep = KSTEP * RS, bstep = KSTEP * plane;
-  // For each tap, the reduction group's channel steps run in groups of 4:
-  // all fragment reads of a group are issued before its MFMAs.
+  const int astep = KSTEP * RS, bstep = KSTEP * pp;
+  // One k-step (KSTEP channels) at a time, all filter taps unrolled inside it
+  // when R and S are compile-time: tap offsets become immediate LDS offsets
+  // and each step exposes R*S*TM*TN independent-enough MFMAs to the
+  // scheduler. The pixel rows of the taps are per-lane bases set up once.
+  int b_row[TN][RC ? RC : 1];
+  if constexpr (RC != 0) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < RC; ++r) b_row[j][r] = b_base[j] + r * wt;
+  }
   auto compute = [&](int stage) {
     const float* Xs = smem + stage * stage_floats;
     const float* As = Xs + a.xs_pad;
-    for (int r = 0; r < R; ++r) {
-      for (int s = 0; s < S; ++s) {
-        const float* ap = As + (r * S + s) + i_begin * astep;
-        const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * bstep;
-        int ii = 0;
-        for (; ii + 4 <= n_i; ii += 4) {
-          float fa[4][TM], fb[4][TN];
+    if constexpr (RC != 0) {
+      constexpr int kUnrollSteps = RC == 1 ? 4 : 1;  // a 1x1 filter has one tap per step
+#pragma unroll kUnrollSteps
+      for (int ii = 0; ii < n_i; ++ii) {
+        const float* ap = As + (i_begin + ii) * astep;
+        const float* bp = Xs + (i_begin + ii) * bstep;
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
+        for (int r = 0; r < RC; ++r) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i) fa[u][i] = ap[a_base[i] + (ii + u) * astep];
+          for (int s = 0; s < RC; ++s) {
+            float fa[TM], fb[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) fb[u][j] = bp[b_base[j] + (ii + u) * bstep];
-          }
+            for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + r * RC + s];
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
+            for (int j = 0; j < TN; ++j) fb[j] = bp[b_row[j][r] + s];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-              for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[u][i], fb[u][j], acc[i][j]);
+              for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[i], fb[j], acc[i][j]);
+          }
         }
-        for (; ii < n_i; ++ii) {
-          float fa[TM], fb[TN];
+      }
+    } else {
+      for (int r = 0; r < R; ++r) {
+        for (int s = 0; s < S; ++s) {
+          const float* ap = As + (r * S + s) + i_begin * astep;
+          const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * bstep;
+          for (int ii = 0; ii < n_i; ++ii) {
+            float fa[TM], fb[TN];
 #pragma unroll
-          for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * astep];
+            for (int i = 0; i < TM; ++i) fa[i] = ap[a_base[i] + ii * astep];
 #pragma unroll
-          for (int j = 0; j < TN; ++j) fb[j] = bp[b_base[j] + ii * bstep];
+            for (int j = 0; j < TN; ++j) fb[j] = bp[b_base[j] + ii * bstep];
 #pragma unroll
-          for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[i], fb[j], acc[i][j]);
+              for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[i], fb[j], acc[i][j]);
+          }
         }
       }
     }

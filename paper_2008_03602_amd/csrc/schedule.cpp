@@ -321,12 +321,19 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const int wt = (tpw - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1;
   // LDS copies move 64 words per wave instruction: the halo as a flat array
   // padded to whole loads of every wave, the filter row by row in 64-word
-  // segments; filter rows get an odd pitch of at least 65 words
+  // segments into rows of at least 64 words
+  // Bank padding (32 banks, half a wave per LDS pass): with 16x16x4 MFMAs a
+  // pass reads 16 filter rows at two k offsets R*S apart and 16 pixels at two
+  // channels, so the row pitch is 2 (mod 32) and the channel pitch 16 (mod 32);
+  // with 32x32x2 a pass reads 32 rows at one k, so the row pitch is odd.
   const int nw = threads / 64;
-  const int64_t xs = (int64_t)cpcp * ht * wt;
+  const int plane = ht * wt;
+  const int pp = mf == 16 ? plane + ((16 - plane) & 31) : plane;
+  const int64_t xs = (int64_t)cpcp * pp;
   const int jw = rs * cpcp;
   const int nseg = (int)cdiv(jw, 64);
-  const int lda = jw >= 64 ? (jw | 1) : 65;
+  const int lrow = std::max(jw, 64);
+  const int lda = mf == 16 ? lrow + ((2 - lrow) & 31) : (lrow | 1);
   g->a_loads = (int)cdiv(xs, 64 * nw);           // halo loads per wave per chunk
   g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);  // filter loads per wave per chunk
   if (g->a_loads > 16) REJECT("too many halo loads per wave");
@@ -343,6 +350,7 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   if (lbytes > kMaxLdsBytes) REJECT("LDS tile too large");
   g->xs_pad = (int)xs_pad;
   g->f_nseg = nseg;
+  g->hpp = pp;
   g->bm = bm;
   g->bn = bn;
   g->cpcp = cpcp;
