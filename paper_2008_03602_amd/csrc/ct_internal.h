@@ -78,7 +78,8 @@ struct Geom {
   int kc, kcp;           // reduction rows per chunk, and padded to whole k-steps
   int cpcp, lda, tph, tpw;  // fp32 MFMA family: padded channels per chunk, filter row pitch, pixel rectangle
   int xs_pad, f_nseg;       // fp32 MFMA family: halo words per stage, 64-word segments per filter row
-  int hpp;                  // fp32 MFMA family: LDS words per halo channel
+  int hpp, hrw, hshift;     // fp32 MFMA family: LDS words per halo channel / row, column shift
+  int vec_h, vec_f;         // fp32 MFMA family: 16-byte copies of the halo / filter
 };
 
 // Validates s on x and fills g. Returns CT_OK or CT_S_INVALID (reason in why).

@@ -37,13 +37,17 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.cps = g.chunks_per_split; a.chunks = g.chunks;
   a.n_halo = g.a_loads; a.n_filt_units = g.bm * g.f_nseg;
   a.xs_pad = g.xs_pad; a.f_nseg = g.f_nseg;
+  // 16-byte copies need 16-byte-aligned tensors (torch allocations are)
+  if ((g.vec_h && ((uintptr_t)xin & 15)) || (g.vec_f && ((uintptr_t)w & 15))) return -1;
   const int T = a.threads;
-  a.pp = g.hpp;
-  a.inv_pp = 1.0f / (float)a.pp;
-  a.inv_wt = 1.0f / (float)a.wt;
+  a.pp = g.hpp; a.rw = g.hrw; a.hshift = g.hshift; a.vec_h = g.vec_h; a.vec_f = g.vec_f;
+  const int vh = g.vec_h ? 4 : 1;
+  const int pu = a.pp / vh, ru = a.rw / vh;
+  a.inv_pu = 1.0f / (float)pu;
+  a.inv_ru = 1.0f / (float)ru;
   a.inv_tpw = 1.0f / (float)a.tpw;
-  a.h_dc = T / a.pp;
-  a.h_drem = T % a.pp;
+  a.h_dc = T / pu;
+  a.h_drem = T % pu;
   a.ny = x.ny;
   IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);
   dim3 grid((unsigned)(o.n * g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.split);

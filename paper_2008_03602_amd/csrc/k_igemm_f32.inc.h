@@ -54,14 +54,17 @@ struct IgF32Args {
   int ht, wt, lda;
   int bm, bn, threads;
   int cps, chunks;
-  int xs_pad;          // halo words per stage: whole wave loads
-  int n_halo;          // halo loads per wave per chunk
-  int n_filt_units;    // filter loads per chunk (all waves): rows x segments
-  int f_nseg;          // 64-word segments per filter row
-  int pp;              // LDS words per halo channel (the plane plus bank padding)
-  // host-precomputed: exact reciprocals for small quotients, and the block
-  // size decomposed over the halo's (channel, word of the channel)
-  float inv_pp, inv_wt, inv_tpw;
+  int xs_pad;          // halo words per stage: whole wave copies
+  int n_halo;          // halo copies per wave per chunk
+  int n_filt_units;    // filter copies per chunk (all waves): rows x segments
+  int f_nseg;          // segments per filter row
+  int pp;              // LDS words per halo channel (the rows plus bank padding)
+  int rw;              // LDS words per halo row
+  int hshift;          // LDS column of input column iw0 (rows start that much earlier)
+  int vec_h, vec_f;    // 1: the halo / filter is copied 16 bytes per lane
+  // host-precomputed, in copy units (1 or 4 words): exact reciprocals of the
+  // units per channel and per row, and the block size over (channel, unit)
+  float inv_pu, inv_ru, inv_tpw;
   int h_dc, h_drem;
   int64_t ny;
 };
@@ -100,6 +103,11 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 __device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 4, off, 0, 0, 0);
 }
+// The same with 16 bytes per lane: lane i fills lds[4i .. 4i+3] (lds and the
+// lane's source 16-byte aligned).
+__device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, 0);
+}
 // Waits for this wave's copies to land in LDS.
 __device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -119,8 +127,8 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int HW = a.H * a.W;
 
   extern __shared__ float smem[];
-  const int cpcp = a.cpcp, bm = a.bm, ht = a.ht, wt = a.wt, lda = a.lda;
-  const int plane = ht * wt, pp = a.pp;
+  const int cpcp = a.cpcp, bm = a.bm, ht = a.ht, lda = a.lda;
+  const int pp = a.pp, rw = a.rw;
   const int jw = cpcp * RS;  // filter words per output channel in a chunk
   const int stage_floats = a.xs_pad + bm * lda;
 
@@ -141,33 +149,44 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int k0 = blockIdx.y * bm, sp = blockIdx.z;
   const int cl = min(a.cpc, a.C);  // channels of x in a chunk
 
-  // ---- halo plan: slot i of this wave copies halo words (i*nw + wave)*64 + lane
-  // of Xs[CPCP][PP]; a word of a channel at or past the plane is bank padding ----
+  // ---- halo plan. Xs[CPCP][PP]: row hh of channel c at c*PP + hh*RW, LDS
+  // column j holding input column iw0 - HSHIFT + j. Copy unit: 1 word, or 4
+  // (16-byte copies: a unit is then wholly inside or wholly outside the
+  // image). Slot i of this wave copies units (i*nw + wave)*64 + lane of the
+  // flat array; a unit past the rows of its channel is bank padding. ----
+  const int vh = a.vec_h ? 4 : 1;
+  const int ru = rw / vh;
   int h_off[kHaloSlots];
   {
-    int c = qdiv(t, a.inv_pp), rem = t - c * pp;
+    const int pu = pp / vh, rows_u = ht * ru;
+    int c = qdiv(t, a.inv_pu), rem = t - c * pu;
 #pragma unroll
     for (int i = 0; i < kHaloSlots; ++i) {
       if (i < a.n_halo) {
-        const int hh = qdiv(rem, a.inv_wt), ww = rem - hh * wt;
-        const int gh = ih0 + hh, gw = iw0 + ww;
-        const bool ok = c < cl && rem < plane && (unsigned)gh < (unsigned)a.H && (unsigned)gw < (unsigned)a.W;
+        const int hh = qdiv(rem, a.inv_ru), col = (rem - hh * ru) * vh;
+        const int gh = ih0 + hh, gw = iw0 - a.hshift + col;
+        const bool ok = c < cl && rem < rows_u && (unsigned)gh < (unsigned)a.H && (unsigned)gw < (unsigned)a.W;
         h_off[i] = ok ? (c * HW + gh * a.W + gw) * 4 : kOob;
-        // advance by T words: (c, rem) += (h_dc, h_drem) with a carry
+        // advance by T units: (c, rem) += (h_dc, h_drem) with a carry
         rem += a.h_drem;
-        const int cr = rem >= pp;
-        rem -= cr ? pp : 0;
+        const int cr = rem >= pu;
+        rem -= cr ? pu : 0;
         c += a.h_dc + cr;
       }
     }
   }
-  // ---- filter plan: slot j of this wave copies 64 words of row m starting at
-  // word f_dst - m*lda, where unit u = j*nw + wave enumerates (m, segment)
-  // row-major. A row shorter than 64 words has a pitch of at least 64 (the
-  // copy's tail lands in the row's padding); a longer row's last segment is
-  // aligned to the row end, overlapping the one before it with the same data. ----
+  // ---- filter plan: slot j of this wave copies one segment (64 units) of row
+  // m, starting at word f_dst - m*lda; unit u = j*nw + wave enumerates
+  // (m, segment) row-major. A row shorter than a segment copies only the
+  // lanes it needs (a 1-word copy lands in padding of rows of at least 64
+  // words); a longer row's last segment is aligned to the row end,
+  // overlapping the one before it with the same data. ----
+  const int vf = a.vec_f ? 4 : 1, seg_len = 64 * vf;
   const int nseg = a.f_nseg;
   const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) / nw : 0;
+  // 1-word copies land in rows of at least 64 words; 16-byte copies of a row
+  // shorter than a segment use only the lanes the row needs
+  const bool f_lane = vf == 1 || lane * 4 < jw;
   int f_off[kFiltSlots], f_dst[kFiltSlots];
   {
     const int dm = nw / nseg, dseg = nw - dm * nseg;
@@ -175,8 +194,8 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 #pragma unroll
     for (int j = 0; j < kFiltSlots; ++j) {
       if (j < n_filt_w) {
-        const int s0 = jw >= 64 ? min(seg * 64, jw - 64) : 0;
-        const int jj = s0 + lane;
+        const int s0 = jw >= seg_len ? min(seg * seg_len, jw - seg_len) : 0;
+        const int jj = s0 + lane * vf;
         f_off[j] = jj < cl * RS ? (m * a.kred + jj) * 4 : kOob;
         f_dst[j] = m * lda + s0;
         seg += dseg;
@@ -199,12 +218,26 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
         make_rsrc(x + ((int64_t)nimg * a.C + c0) * HW, (int64_t)cl * HW * 4);
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)k0 * a.kred + (int64_t)c0 * RS,
                                                 ((int64_t)(a.K - k0) * a.kred - (int64_t)c0 * RS) * 4);
+    if (a.vec_h) {
 #pragma unroll
-    for (int i = 0; i < kHaloSlots; ++i)
-      if (i < a.n_halo) copy_to_lds(rx, xs + (i * nw + wave) * 64, h_off[i]);
+      for (int i = 0; i < kHaloSlots; ++i)
+        if (i < a.n_halo) copy16_to_lds(rx, xs + (i * nw + wave) * 256, h_off[i]);
+    } else {
 #pragma unroll
-    for (int j = 0; j < kFiltSlots; ++j)
-      if (j < n_filt_w) copy_to_lds(rw, as + f_dst[j], f_off[j]);
+      for (int i = 0; i < kHaloSlots; ++i)
+        if (i < a.n_halo) copy_to_lds(rx, xs + (i * nw + wave) * 64, h_off[i]);
+    }
+    if (f_lane) {
+      if (a.vec_f) {
+#pragma unroll
+        for (int j = 0; j < kFiltSlots; ++j)
+          if (j < n_filt_w) copy16_to_lds(rw, as + f_dst[j], f_off[j]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < kFiltSlots; ++j)
+          if (j < n_filt_w) copy_to_lds(rw, as + f_dst[j], f_off[j]);
+      }
+    }
   };
 
   V acc[TM][TN];
@@ -224,7 +257,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   for (int j = 0; j < TN; ++j) {
     const int q = n_off + j * MF + lrow;
     const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
-    b_base[j] = kg * pp + (pr * sh) * wt + pc * sw;
+    b_base[j] = kg * pp + (pr * sh) * rw + pc * sw + a.hshift;
   }
   const int n_i = cpcp / KSTEP / a.wsp;  // k-steps per tap for this reduction group
   const int i_begin = wg * n_i;
@@ -238,7 +271,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < RC; ++r) b_row[j][r] = b_base[j] + r * wt;
+      for (int r = 0; r < RC; ++r) b_row[j][r] = b_base[j] + r * rw;
   }
   auto compute = [&](int stage) {
     const float* Xs = smem + stage * stage_floats;
@@ -269,7 +302,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       for (int r = 0; r < R; ++r) {
         for (int s = 0; s < S; ++s) {
           const float* ap = As + (r * S + s) + i_begin * astep;
-          const float* bp = Xs + (r * dh) * wt + s * dw + i_begin * bstep;
+          const float* bp = Xs + (r * dh) * rw + s * dw + i_begin * bstep;
           for (int ii = 0; ii < n_i; ++ii) {
             float fa[TM], fb[TN];
 #pragma unroll

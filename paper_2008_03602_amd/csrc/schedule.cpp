@@ -319,26 +319,45 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const int rs = o.r * o.s;
   const int ht = (tph - 1) * o.stride_h + (o.r - 1) * o.dil_h + 1;
   const int wt = (tpw - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1;
-  // LDS copies move 64 words per wave instruction: the halo as a flat array
-  // padded to whole loads of every wave, the filter row by row in 64-word
-  // segments into rows of at least 64 words
+  // Copies move 64 units per wave instruction (a unit is 1 word, or 4 words
+  // with 16-byte copies): the halo as a flat array padded to whole copies of
+  // every wave, the filter row by row in 64-unit segments.
+  // Halo: 16-byte copies need every unit wholly inside or outside the image,
+  // so W and the tile's first column are multiples of 4 (rows then start
+  // HSHIFT columns before the tile's first input column).
+  // Filter: 16-byte copies need 16-byte-aligned rows in global memory and LDS.
   // Bank padding (32 banks, half a wave per LDS pass): with 16x16x4 MFMAs a
   // pass reads 16 filter rows at two k offsets R*S apart and 16 pixels at two
-  // channels, so the row pitch is 2 (mod 32) and the channel pitch 16 (mod 32);
-  // with 32x32x2 a pass reads 32 rows at one k, so the row pitch is odd.
+  // channels, so the channel pitch is 16 (mod 32) and the row pitch 2 (mod 32)
+  // (4 (mod 8) for 16-byte rows: a 2-way conflict); with 32x32x2 a pass reads
+  // 32 rows at one k, so the row pitch is odd.
   const int nw = threads / 64;
-  const int plane = ht * wt;
-  const int pp = mf == 16 ? plane + ((16 - plane) & 31) : plane;
-  const int64_t xs = (int64_t)cpcp * pp;
+  const int cl = std::min<int>(cpc, (int)x.cg);
+  const bool vec_h = o.w % 4 == 0 && (tpw * o.stride_w) % 4 == 0;
+  const int hshift = vec_h ? (4 - o.pad_w % 4) % 4 : 0;
+  const int rw = vec_h ? (int)cdiv(hshift + wt, 4) * 4 : wt;
+  const int rows = ht * rw;
+  const int pp = mf == 16 ? rows + ((16 - rows) & 31) : (vec_h ? (int)cdiv(rows, 4) * 4 : rows);
+  const int vh = vec_h ? 4 : 1;
   const int jw = rs * cpcp;
-  const int nseg = (int)cdiv(jw, 64);
-  const int lrow = std::max(jw, 64);
-  const int lda = mf == 16 ? lrow + ((2 - lrow) & 31) : (lrow | 1);
-  g->a_loads = (int)cdiv(xs, 64 * nw);           // halo loads per wave per chunk
-  g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);  // filter loads per wave per chunk
-  if (g->a_loads > 16) REJECT("too many halo loads per wave");
-  if (g->b_loads > 16) REJECT("too many filter loads per wave");
-  const int64_t xs_pad = (int64_t)g->a_loads * 64 * nw;
+  const bool vec_f = mf == 16 && jw % 4 == 0 && x.kred % 4 == 0 && (cl * rs) % 4 == 0 &&
+                     (cpc >= x.cg || (cpc * rs) % 4 == 0);
+  const int vf = vec_f ? 4 : 1;
+  const int nseg = (int)cdiv(jw, 64 * vf);
+  int lda;
+  if (vec_f) {
+    const int l4 = (int)cdiv(jw, 4) * 4;
+    lda = (l4 / 4) % 2 ? l4 : l4 + 4;
+  } else {
+    const int lrow = std::max(jw, 64);
+    lda = mf == 16 ? lrow + ((2 - lrow) & 31) : (lrow | 1);
+  }
+  const int64_t units = (int64_t)cpcp * (pp / vh);
+  g->a_loads = (int)cdiv(units, 64 * nw);            // halo copies per wave per chunk
+  g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);    // filter copies per wave per chunk
+  if (g->a_loads > 16) REJECT("too many halo copies per wave");
+  if (g->b_loads > 16) REJECT("too many filter copies per wave");
+  const int64_t xs_pad = (int64_t)g->a_loads * 64 * nw * vh;
   if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
     REJECT("tensor too large for 32-bit buffer offsets");
   const int64_t chunks = cdiv(x.cg, cpc);
@@ -351,6 +370,10 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   g->xs_pad = (int)xs_pad;
   g->f_nseg = nseg;
   g->hpp = pp;
+  g->hrw = rw;
+  g->hshift = hshift;
+  g->vec_h = vec_h;
+  g->vec_f = vec_f;
   g->bm = bm;
   g->bn = bn;
   g->cpcp = cpcp;
