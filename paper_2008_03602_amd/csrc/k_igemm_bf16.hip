@@ -8,8 +8,9 @@
 //
 // A block owns a BM x BN tile (BM = WM*TM*MF pixels, BN = WN*TN*MF
 // channels), one wave per WM x WN sub-tile. LDS = 0 loads each wave's
-// fragments straight from global memory, issuing a whole reduction chunk
-// (KC) of loads before its MFMAs; LDS = 1 stages the chunk's A and B tiles
+// fragments straight from global memory, a whole reduction chunk (KC) at a
+// time, the next chunk's loads in flight during the current chunk's MFMAs
+// (two register sets, for TM + TN <= 4); LDS = 1 stages the chunk's A and B tiles
 // in LDS with coalesced 16-byte loads shared by the block. SPLIT > 1 spreads
 // contiguous chunk ranges over grid.y (partials added in split order by a
 // second kernel). SWZ = 1 renumbers blocks so that the tiles each XCD
@@ -126,9 +127,12 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
       boff[j] = bok[j] ? n * a.C : 0;
     }
     const int steps = a.kc / KSTEP;
-    for (int ch = ch_begin; ch < ch_end; ++ch) {
+    // The fragments of chunk ch+1 are loaded into a second register set
+    // while the MFMAs of chunk ch run (two sets, used alternately).
+    using FragA = bf16x8[kBf16MaxSteps][TM];
+    using FragB = bf16x8[kBf16MaxSteps][TN];
+    auto load_chunk = [&](int ch, FragA& fa, FragB& fb) {
       const int kr0 = ch * a.kc;
-      bf16x8 fa[kBf16MaxSteps][TM], fb[kBf16MaxSteps][TN];
 #pragma unroll
       for (int st = 0; st < kBf16MaxSteps; ++st) {
         const int k = kr0 + st * KSTEP + kq;
@@ -138,6 +142,8 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
 #pragma unroll
         for (int j = 0; j < TN; ++j) fb[st][j] = load8(w, (int64_t)boff[j] + k, kok && bok[j]);
       }
+    };
+    auto mma_chunk = [&](const FragA& fa, const FragB& fb) {
 #pragma unroll
       for (int st = 0; st < kBf16MaxSteps; ++st) {
         if (st < steps) {
@@ -146,6 +152,26 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
 #pragma unroll
             for (int j = 0; j < TN; ++j) acc[i][j] = M::op(fa[st][i], fb[st][j], acc[i][j]);
         }
+      }
+    };
+    if constexpr (TM + TN <= 4) {
+      FragA fa0, fa1;
+      FragB fb0, fb1;
+      if (ch_begin < ch_end) load_chunk(ch_begin, fa0, fb0);
+      for (int ch = ch_begin; ch < ch_end; ch += 2) {
+        if (ch + 1 < ch_end) load_chunk(ch + 1, fa1, fb1);
+        mma_chunk(fa0, fb0);
+        if (ch + 1 >= ch_end) break;
+        if (ch + 2 < ch_end) load_chunk(ch + 2, fa0, fb0);
+        mma_chunk(fa1, fb1);
+      }
+    } else {
+      // larger fragment sets: one set (two would spill registers)
+      FragA fa0;
+      FragB fb0;
+      for (int ch = ch_begin; ch < ch_end; ++ch) {
+        load_chunk(ch, fa0, fb0);
+        mma_chunk(fa0, fb0);
       }
     }
   } else {
