@@ -48,6 +48,15 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.inv_tpw = 1.0f / (float)a.tpw;
   a.h_dc = T / pu;
   a.h_drem = T % pu;
+  const int nw = T / 64;
+  a.inv_tiles_hw = 1.0f / (float)(g.tiles_h * g.tiles_w);
+  a.inv_tiles_w = 1.0f / (float)g.tiles_w;
+  a.inv_nseg = 1.0f / (float)g.f_nseg;
+  a.f_dm = nw / g.f_nseg;
+  a.f_dseg = nw % g.f_nseg;
+  a.lg_wpg = __builtin_ctz(a.wm * a.wn);
+  a.lg_wn = __builtin_ctz(a.wn);
+  a.lg_nw = __builtin_ctz(nw);
   a.ny = x.ny;
   IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);
   dim3 grid((unsigned)(o.n * g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.split);

@@ -66,6 +66,9 @@ struct IgF32Args {
   // units per channel and per row, and the block size over (channel, unit)
   float inv_pu, inv_ru, inv_tpw;
   int h_dc, h_drem;
+  float inv_tiles_hw, inv_tiles_w, inv_nseg;
+  int f_dm, f_dseg;            // the wave count over (filter row, segment)
+  int lg_wpg, lg_wn, lg_nw;    // log2 of WM*WN, WN and the wave count
   int64_t ny;
 };
 
@@ -134,16 +137,17 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 
   const int t = threadIdx.x, lane = t & 63, wave = wave_id();
   const int nw = a.threads >> 6;
+  // WM, WN, WS and the wave count are powers of two: shifts, not divisions
   const int wpg = a.wm * a.wn;
-  const int wg = wave / wpg, wi = wave - wg * wpg;
-  const int wmi = wi / a.wn, wni = wi - wmi * a.wn;
+  const int wg = wave >> a.lg_wpg, wi = wave & (wpg - 1);
+  const int wmi = wi >> a.lg_wn, wni = wi & ((1 << a.lg_wn) - 1);
   const int m_off = wmi * TM * MF, n_off = wni * TN * MF;
 
   // block -> (image, pixel rectangle), output-channel tile, split
   const int tiles_hw = a.tiles_h * a.tiles_w;
-  const int nimg = blockIdx.x / tiles_hw;
+  const int nimg = qdiv(blockIdx.x, a.inv_tiles_hw);
   const int trem = blockIdx.x - nimg * tiles_hw;
-  const int th = trem / a.tiles_w, tw = trem - th * a.tiles_w;
+  const int th = qdiv(trem, a.inv_tiles_w), tw = trem - th * a.tiles_w;
   const int oh0 = th * a.tph, ow0 = tw * a.tpw;
   const int ih0 = oh0 * sh - ph, iw0 = ow0 * sw - pw;
   const int k0 = blockIdx.y * bm, sp = blockIdx.z;
@@ -183,14 +187,14 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   // overlapping the one before it with the same data. ----
   const int vf = a.vec_f ? 4 : 1, seg_len = 64 * vf;
   const int nseg = a.f_nseg;
-  const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) / nw : 0;
+  const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) >> a.lg_nw : 0;
   // 1-word copies land in rows of at least 64 words; 16-byte copies of a row
   // shorter than a segment use only the lanes the row needs
   const bool f_lane = vf == 1 || lane * 4 < jw;
   int f_off[kFiltSlots], f_dst[kFiltSlots];
   {
-    const int dm = nw / nseg, dseg = nw - dm * nseg;
-    int m = wave / nseg, seg = wave - (wave / nseg) * nseg;
+    const int dm = a.f_dm, dseg = a.f_dseg;  // nw = dm*nseg + dseg
+    int m = qdiv(wave, a.inv_nseg), seg = wave - m * nseg;
 #pragma unroll
     for (int j = 0; j < kFiltSlots; ++j) {
       if (j < n_filt_w) {

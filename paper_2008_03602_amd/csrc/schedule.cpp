@@ -387,7 +387,8 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   g->tiles_k = cdiv(o.k, bm);
   g->tiles_n = split;
   if (g->tiles_k > 65535) REJECT("grid too large");
-  if ((int64_t)o.n * g->tiles_h * g->tiles_w >= ((int64_t)1 << 31)) REJECT("grid too large");
+  // the kernel splits blockIdx.x with an fp32 reciprocal, exact below 2^22
+  if ((int64_t)o.n * g->tiles_h * g->tiles_w >= ((int64_t)1 << 22)) REJECT("grid too large");
   g->threads = threads;
   g->lds_bytes = (int)lbytes;
   g->blocks = (int64_t)o.n * g->tiles_h * g->tiles_w * g->tiles_k * split;
