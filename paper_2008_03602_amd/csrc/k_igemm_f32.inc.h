@@ -45,6 +45,8 @@ namespace ct {
 
 constexpr int kHaloSlots = 16;  // halo loads per wave per chunk (max)
 constexpr int kFiltSlots = 16;  // filter loads per wave per chunk (max)
+constexpr int kRegCopies = 4;   // register-staged 16-byte copies of each kind per wave (max)
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct IgF32Args {
   int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
@@ -99,6 +101,10 @@ constexpr int kOob = 0x7FFFFFF0;  // byte offset beyond every buffer: reads as 0
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// 16 bytes at byte offset off of r (0 past the buffer's range)
+__device__ __forceinline__ f32x4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -213,15 +219,17 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int ch_end = min(a.chunks, ch_begin + a.cps);
 
   // start the copies of chunk ch into LDS stage `stage`
+  // x: this image's channels [c0, c0 + cl); w: rows [k0, K) from column c0*RS
+  auto rsrc_x = [&](int c0) { return make_rsrc(x + ((int64_t)nimg * a.C + c0) * HW, (int64_t)cl * HW * 4); };
+  auto rsrc_w = [&](int c0) {
+    return make_rsrc(w + (int64_t)k0 * a.kred + (int64_t)c0 * RS,
+                     ((int64_t)(a.K - k0) * a.kred - (int64_t)c0 * RS) * 4);
+  };
   auto issue = [&](int ch, int stage) {
     const int c0 = ch * a.cpc;
     float* xs = smem + stage * stage_floats;
     float* as = xs + a.xs_pad;
-    // x: this image's channels [c0, c0 + cl); w: rows [k0, K) from column c0*RS
-    const __amdgpu_buffer_rsrc_t rx =
-        make_rsrc(x + ((int64_t)nimg * a.C + c0) * HW, (int64_t)cl * HW * 4);
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)k0 * a.kred + (int64_t)c0 * RS,
-                                                ((int64_t)(a.K - k0) * a.kred - (int64_t)c0 * RS) * 4);
+    const __amdgpu_buffer_rsrc_t rx = rsrc_x(c0), rw = rsrc_w(c0);
     if (a.vec_h) {
 #pragma unroll
       for (int i = 0; i < kHaloSlots; ++i)
@@ -323,6 +331,35 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   };
 
+  // STAGES = 2 with 16-byte copies and at most kRegCopies of each kind per
+  // wave: the next chunk goes through registers instead (16-byte loads that
+  // stay in flight during the MFMAs, stored to LDS after them). A copy
+  // straight to LDS holds its wave about one L2 round trip on this device,
+  // so several of them in a row stall the wave that should be issuing MFMAs.
+  const bool via_regs = STAGES == 2 && a.vec_h && a.vec_f && a.n_halo <= kRegCopies &&
+                        ((a.n_filt_units + nw - 1) >> a.lg_nw) <= kRegCopies;
+  f32x4 rh[kRegCopies], rf[kRegCopies];
+  auto load_regs = [&](int ch) {
+    const int c0 = ch * a.cpc;
+    const __amdgpu_buffer_rsrc_t rx = rsrc_x(c0), rw = rsrc_w(c0);
+#pragma unroll
+    for (int i = 0; i < kRegCopies; ++i)
+      if (i < a.n_halo) rh[i] = bload16(rx, h_off[i]);
+#pragma unroll
+    for (int j = 0; j < kRegCopies; ++j)
+      if (j < n_filt_w && f_lane) rf[j] = bload16(rw, f_off[j]);
+  };
+  auto store_regs = [&](int stage) {
+    float* xs = smem + stage * stage_floats;
+    float* as = xs + a.xs_pad;
+#pragma unroll
+    for (int i = 0; i < kRegCopies; ++i)
+      if (i < a.n_halo) *(f32x4*)(xs + (i * nw + wave) * 256 + lane * 4) = rh[i];
+#pragma unroll
+    for (int j = 0; j < kRegCopies; ++j)
+      if (j < n_filt_w && f_lane) *(f32x4*)(as + f_dst[j] + lane * 4) = rf[j];
+  };
+
   if constexpr (STAGES == 1) {
     for (int ch = ch_begin; ch < ch_end; ++ch) {
       issue(ch, 0);
@@ -330,6 +367,20 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       __syncthreads();
       compute(0);
       __syncthreads();  // the next chunk's copies overwrite this stage
+    }
+  } else if (via_regs) {
+    if (ch_begin < ch_end) {
+      issue(ch_begin, 0);
+      wait_copies();
+    }
+    __syncthreads();
+    for (int ch = ch_begin; ch < ch_end; ++ch) {
+      const int cur = (ch - ch_begin) & 1;
+      const bool more = ch + 1 < ch_end;
+      if (more) load_regs(ch + 1);
+      compute(cur);
+      if (more) store_regs(cur ^ 1);  // the stage chunk ch-1 used, free since the last barrier
+      __syncthreads();
     }
   } else {
     if (ch_begin < ch_end) issue(ch_begin, 0);
