@@ -182,7 +182,10 @@ int ct_sample(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_i
 /* ---- running and timing (section 2.1 stage 3, "profile") ---- */
 
 /* Run schedule s once on op: y = conv2d(x, w). cu_mask = NULL uses all CUs.
- * Returns after the run has completed. CT_E_ARG if s is invalid for op. */
+ * Returns after the run has completed. CT_E_ARG if s is invalid for op, or
+ * if s copies 16 bytes per lane (IGEMM_F32 on suitable shapes) and x or w is
+ * not 16-byte aligned; measurement entry points report the latter as
+ * CT_S_LAUNCH for that candidate. */
 int conv2d_run(const ct_op *op, const ct_schedule *s, const void *x, const void *w, void *y,
                const uint32_t *cu_mask, int words);
 

@@ -86,6 +86,8 @@ struct Geom {
 int compute_geom(const OpX& x, const ct_schedule& s, Geom* g, std::string* why);
 
 // ---- kernel launchers (one per family, in the .hip files) ----
+// Return 0, -1 on a HIP launch error, or -2 when the arguments are refused
+// (reason given to set_error).
 // ws: workspace of at least g.ws_floats floats when g.split > 1.
 int launch_direct_f32(const OpX& x, const ct_schedule& s, const Geom& g, const void* xin,
                       const void* w, void* y, float* ws, void* stream);

@@ -38,7 +38,10 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.n_halo = g.a_loads; a.n_filt_units = g.bm * g.f_nseg;
   a.xs_pad = g.xs_pad; a.f_nseg = g.f_nseg;
   // 16-byte copies need 16-byte-aligned tensors (torch allocations are)
-  if ((g.vec_h && ((uintptr_t)xin & 15)) || (g.vec_f && ((uintptr_t)w & 15))) return -1;
+  if ((g.vec_h && ((uintptr_t)xin & 15)) || (g.vec_f && ((uintptr_t)w & 15))) {
+    set_error("igemm_f32: this schedule copies 16 bytes per lane and needs 16-byte-aligned x and w");
+    return -2;
+  }
   const int T = a.threads;
   a.pp = g.hpp; a.rw = g.hrw; a.hshift = g.hshift; a.vec_h = g.vec_h; a.vec_f = g.vec_f;
   const int vh = g.vec_h ? 4 : 1;

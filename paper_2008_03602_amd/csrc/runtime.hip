@@ -516,7 +516,9 @@ int conv2d_run(const ct_op* op, const ct_schedule* s, const void* x, const void*
   StreamCtx* c = nullptr;
   if ((rc = get_ctx(key, &c))) return rc;
   if ((rc = ensure_ws(c, g.ws_floats))) return rc;
-  if (launch_once(ox, *s, g, x, w, y, c->ws, c->stream) != 0) return hip_fail("conv2d_run launch", hipGetLastError());
+  const int lrc = launch_once(ox, *s, g, x, w, y, c->ws, c->stream);
+  if (lrc == -2) return CT_E_ARG;  // the launcher refused the arguments (reason already set)
+  if (lrc != 0) return hip_fail("conv2d_run launch", hipGetLastError());
   HIP_TRY(hipStreamSynchronize(c->stream));
   return CT_OK;
 }

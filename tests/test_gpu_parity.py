@@ -5,6 +5,8 @@ tiles with ragged tails (H, W, K and C not multiples of the tile sizes, C = 3,
 stride 2, 7x7 filters). Each case runs a seeded sample of schedules from the
 op's valid candidate space.
 """
+import random
+
 import numpy as np
 import pytest
 import torch
@@ -28,6 +30,13 @@ DW_OPS = [
     W.conv("dw_s2", 3, 24, 17, 24, 3, 2, 1, groups=24),
     W.Op("dw5x5", 1, 8, 10, 10, 8, 5, 5, 1, 1, 2, 2, 1, 1, 8, 0, 0),
 ]
+# shapes where IGEMM_F32 copies 16 bytes per lane (W a multiple of 4), with ragged tiles
+VEC_OPS = [
+    W.conv("vec3x3", 1, 24, 20, 40, 3, 1),
+    W.conv("vec3x3s2", 1, 16, 28, 24, 3, 2),
+    W.conv("vec1x1", 2, 32, 12, 20, 1, 1, 0),
+    W.Op("vec_rect", 2, 12, 9, 24, 20, 3, 3, 1, 1, 1, 1, 1, 1, 1, 0, 0),
+]
 BF_OPS = [
     W.conv("pwbf_odd", 2, 24, 9, 40, 1, 1, 0, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC),
     W.conv("pwbf_c96", 1, 96, 11, 24, 1, 1, 0, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC),
@@ -41,11 +50,15 @@ def _device():
     yield
 
 
-def _run_sample(op, n_sched, seed, dist="uniform", int_range=2, exact=False):
+def _run_sample(op, n_sched, seed, dist="uniform", int_range=2, exact=False, family=None):
     x, w = make_inputs(op, dist, seed=seed, int_range=int_range)
     ref, a = reference(op, x, w)
     xd, wd, yd = to_device(op, x, w)
-    scheds = L.ct_sample(op, seed, 99, 0, n_sched)
+    if family is None:
+        scheds = L.ct_sample(op, seed, 99, 0, n_sched)
+    else:  # a seeded sample of one family's valid schedules
+        space = [s for s in L.ct_valid_space(op) if s.family == family]
+        scheds = random.Random(seed).sample(space, min(n_sched, len(space)))
     assert len(scheds) > 0
     fams = set()
     for s in scheds:
@@ -67,6 +80,36 @@ def _run_sample(op, n_sched, seed, dist="uniform", int_range=2, exact=False):
 def test_fp32_families_match_oracle(op):
     fams = _run_sample(op, 24, seed=11)
     assert fams <= {W.FAM_DIRECT_F32, W.FAM_IGEMM_F32}
+
+
+@pytest.mark.parametrize("op", F32_OPS + VEC_OPS, ids=lambda o: o.name)
+def test_fp32_mfma_schedules_match_oracle(op):
+    # 24 schedules of the MFMA family alone: both staging depths, 1- and
+    # 16-byte copies, register double buffering, reduction groups and splits
+    assert _run_sample(op, 24, seed=14, family=W.FAM_IGEMM_F32) == {W.FAM_IGEMM_F32}
+
+
+def test_misaligned_tensors_are_refused_by_16_byte_schedules():
+    op = VEC_OPS[0]
+    x, w = make_inputs(op, "uniform", seed=3)
+    ref, a = reference(op, x, w)
+    xd, wd, yd = to_device(op, x, w)
+    buf = torch.empty(xd.numel() + 4, dtype=torch.float32, device=xd.device)
+    xm = buf[1:1 + xd.numel()].view(op.x_shape())  # 4 bytes past a 16-byte boundary
+    xm.copy_(xd)
+    space = L.ct_valid_space(op)
+    vec = next(s for s in space if s.family == W.FAM_IGEMM_F32)
+    direct = next(s for s in space if s.family == W.FAM_DIRECT_F32)
+    note("misaligned x: " + sched_str(vec))
+    with pytest.raises(L.CtError) as e:
+        L.conv2d_run(op, vec, xm, wd, yd)
+    assert e.value.code == L.CT_E_ARG and "aligned" in str(e.value)
+    lat, st = L.measure_candidates_mask(op, [vec, direct], L.ct_cu_mask(1.0, 0), L.make_opts(1, 1, 2, 2),
+                                        xm, wd, yd)
+    assert list(st) == [L.S_LAUNCH, L.S_OK]
+    yd.fill_(float("nan"))
+    L.conv2d_run(op, direct, xm, wd, yd)
+    check_close(op, yd.cpu().numpy(), ref, a, "misaligned x, direct schedule")
 
 
 @pytest.mark.parametrize("op", DW_OPS, ids=lambda o: o.name)
