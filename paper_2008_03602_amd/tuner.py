@@ -262,6 +262,27 @@ def cross_eval_regret(matrices: Dict[str, list], fractions: Sequence[float]) -> 
     return (acc / max(len(matrices), 1)).tolist()
 
 
+def model_aggregates(matrices: Dict[str, list], fractions: Sequence[float]) -> dict:
+    """Model-level view of the cross-evaluation (the paper's Tables 1-3).
+
+    total[f][g] = sum over layers of multiplicity x M[f][g]: the model's conv
+    time at share g when every layer runs the schedule tuned at share f.
+    best[g] = the same with each layer's best winner for g. The sweet spot is
+    the tuning share whose totals are closest to best on average over g."""
+    n = len(fractions)
+    total = np.zeros((n, n))
+    best = np.zeros(n)
+    for name, M in matrices.items():
+        M = np.asarray(M, dtype=np.float64)
+        k = W.multiplicity(name)
+        total += k * M
+        best += k * M.min(axis=0)
+    ratio = total / best[None, :]
+    mean = ratio.mean(axis=1)
+    return {"total_us": total.tolist(), "best_us": best.tolist(), "ratio_to_best": ratio.tolist(),
+            "mean_ratio_per_tuning_share": mean.tolist(), "sweet_spot": float(fractions[int(np.argmin(mean))])}
+
+
 def find_layer(name: str):
     """(op, config, layer position) of a named layer of configurations 1-5."""
     for cid in range(1, 6):
@@ -363,6 +384,12 @@ def main(argv=None) -> int:
               "latency / best latency in the column):", flush=True)
         for f, row in zip(cfg.fractions, report["cross_eval_regret"]):
             print("  %5.3f: %s" % (f, " ".join("%6.3f" % v for v in row)), flush=True)
+        agg = model_aggregates(report["cross_eval"], cfg.fractions)
+        report["model"] = agg
+        print("model conv time / best, by tuning share (rows) and run share (columns):", flush=True)
+        for f, row in zip(cfg.fractions, agg["ratio_to_best"]):
+            print("  %5.3f: %s" % (f, " ".join("%6.3f" % v for v in row)), flush=True)
+        print("sweet spot (lowest mean ratio): tuned at %.3f" % agg["sweet_spot"], flush=True)
     if a.out:
         with open(a.out, "w") as fh:
             json.dump(report, fh, indent=1)

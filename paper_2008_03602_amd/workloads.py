@@ -149,6 +149,22 @@ def resnet50(n: int = 1) -> List[Op]:
     return [conv("r50.%d" % (i + 1), n, c, h, k, rs, s) for i, (c, h, k, rs, s) in enumerate(spec)]
 
 
+# How many convolutions of the network have each distinct shape (ResNet-18
+# under the four-projection reading: 21 convolutions; ResNet-50 bottlenecks,
+# stem excluded: 52). Used to weigh per-layer latencies into a model total.
+MULTIPLICITY = {
+    "r18.1": 1, "r18.2": 4, "r18.3": 1, "r18.4": 1, "r18.5": 3, "r18.6": 1,
+    "r18.7": 1, "r18.8": 3, "r18.9": 1, "r18.10": 1, "r18.11": 3, "r18.12": 1,
+    **{"r50.%d" % (i + 1): m for i, m in enumerate(
+        [1, 3, 4, 2, 1, 1, 4, 1, 3, 3, 1, 1, 6, 1, 5, 5, 1, 1, 3, 1, 2, 2])},
+}
+
+
+def multiplicity(name: str) -> int:
+    """Occurrences of a layer shape in its network (1 if not tabulated)."""
+    return MULTIPLICITY.get(name, 1)
+
+
 def mobilenet_v2_depthwise(n: int = 16) -> List[Op]:
     spec = [(32, 112, 1), (96, 112, 2), (144, 56, 1), (144, 56, 2), (192, 28, 1), (192, 28, 2),
             (384, 14, 1), (576, 14, 1), (576, 14, 2), (960, 7, 1)]
