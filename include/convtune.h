@@ -271,6 +271,66 @@ int ct_cross_eval(const ct_op *op, const ct_schedule *s, int n_sched,
                   const uint32_t *masks, int n_masks, int words,
                   const ct_measure_opts *o, const void *x, const void *w, void *y, float *M);
 
+/* ---- guided search (section 2.1, stage 4: an exploration algorithm steered
+ *      by a cost model trained on the profiled configurations; early stop) ---- */
+
+typedef struct ct_search_opts {
+    uint64_t seed;       /* all random choices derive from it (splitmix64)            */
+    int32_t batch;       /* candidates proposed and measured per round (>= 1)         */
+    int32_t budget;      /* most candidates measured in total (>= 1)                  */
+    int32_t patience;    /* stop after this many measured candidates in a row that do */
+                         /* not improve the best stage-1 latency by more than eps;    */
+                         /* 0 = never stop early                                       */
+    int32_t sa_chains;   /* simulated-annealing chains per round                      */
+    int32_t sa_steps;    /* steps per chain per round                                 */
+    float explore;       /* share of each batch drawn at random from the unmeasured   */
+                         /* space (the rest: the cost model's best unmeasured states) */
+    float eps;           /* relative improvement that resets the patience count       */
+    float sa_temp;       /* starting temperature, in units of log latency; it falls   */
+                         /* linearly to 0 over a chain                                 */
+} ct_search_opts;
+
+typedef struct ct_search_result {
+    int32_t n_measured;     /* candidates measured (<= budget)                        */
+    int32_t rounds;
+    int32_t stopped_early;  /* 1 if the patience rule ended the search                */
+    int32_t winner;         /* index into the measured list, -1 if none measured OK   */
+    float winner_lat_us;    /* the winner's stage-2 latency                           */
+    float pad_;
+    double propose_s;       /* host seconds spent proposing                           */
+    double measure_s;       /* host seconds spent in measurement calls                */
+} ct_search_result;
+
+/* Next batch of a guided search (host only, no device work). The cost model
+ * is fitted on the n_measured schedules measured so far (status CT_S_OK ones
+ * only): per kernel family, ridge regression of log latency on a one-hot code
+ * of the knob values plus launch-geometry features. so->sa_chains annealing
+ * chains of so->sa_steps steps each (half start at the best measured
+ * schedules of each family in turn, half at random valid ones; a step moves
+ * one knob to a neighbouring value) walk the predicted latency; the
+ * best-predicted unmeasured states they visit fill the batch, except a share
+ * so->explore of it (all of it when nothing has been measured OK yet) drawn
+ * at random: the applicable kernel families in turn, uniformly within each,
+ * so a small family is explored as much as a large one. Random draws that hit
+ * measured schedules are redrawn. Writes min(cap, so->batch) distinct valid
+ * schedules not among `measured` (fewer once the space runs out) to out,
+ * count in *n_out. Same inputs and round give the same output. */
+int ct_search_propose(const ct_op *op, const ct_schedule *measured, const float *lat_us, const int32_t *status,
+                      int n_measured, const ct_search_opts *so, int32_t round, ct_schedule *out, int32_t cap,
+                      int32_t *n_out);
+
+/* Guided tuning of one op on a CU mask: rounds of ct_search_propose and
+ * stage-1 measurement until so->budget candidates are measured, the space
+ * runs out, or the patience rule fires; then the top_t by stage-1 latency are
+ * re-measured with stage2 and the winner chosen by ct_select_winner with eps
+ * (position = index in the measured list). measured, lat_us and status are
+ * caller arrays of so->budget entries and receive every measured candidate in
+ * order. With CT_PROGRESS set, one line per round goes to stderr. */
+int ct_search(const ct_op *op, const ct_search_opts *so, const uint32_t *cu_mask, int words,
+              const ct_measure_opts *stage1, const ct_measure_opts *stage2, int32_t top_t, float eps,
+              const void *x, const void *w, void *y, ct_schedule *measured, float *lat_us, int32_t *status,
+              ct_search_result *res);
+
 /* ---- probes (support for masks and rooflines) ---- */
 
 /* Launch `blocks` one-wave blocks on the mask; each records the hardware

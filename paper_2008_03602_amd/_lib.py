@@ -66,6 +66,16 @@ class ct_client(ctypes.Structure):
                 ("n_measured", c_i64)]
 
 
+class ct_search_opts(ctypes.Structure):
+    _fields_ = [("seed", c_u64), ("batch", c_i32), ("budget", c_i32), ("patience", c_i32), ("sa_chains", c_i32),
+                ("sa_steps", c_i32), ("explore", c_f32), ("eps", c_f32), ("sa_temp", c_f32)]
+
+
+class ct_search_result(ctypes.Structure):
+    _fields_ = [("n_measured", c_i32), ("rounds", c_i32), ("stopped_early", c_i32), ("winner", c_i32),
+                ("winner_lat_us", c_f32), ("pad_", c_f32), ("propose_s", c_f64), ("measure_s", c_f64)]
+
+
 _SIGS = {
     "ct_init": (c_i32, [c_i32]),
     "ct_num_cus": (c_i32, []),
@@ -96,6 +106,11 @@ _SIGS = {
                                P(ct_measure_opts), c_f32, P(c_i32)]),
     "ct_cross_eval": (c_i32, [P(ct_op), P(ct_schedule), c_i32, P(c_u32), c_i32, c_i32, P(ct_measure_opts),
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, P(c_f32)]),
+    "ct_search_propose": (c_i32, [P(ct_op), P(ct_schedule), P(c_f32), P(c_i32), c_i32, P(ct_search_opts), c_i32,
+                                  P(ct_schedule), c_i32, P(c_i32)]),
+    "ct_search": (c_i32, [P(ct_op), P(ct_search_opts), P(c_u32), c_i32, P(ct_measure_opts), P(ct_measure_opts),
+                          c_i32, c_f32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, P(ct_schedule), P(c_f32),
+                          P(c_i32), P(ct_search_result)]),
     "ct_probe_cus": (c_i32, [P(c_u32), c_i32, c_i32, P(c_i32), c_i32, P(c_i32)]),
     "ct_probe_empty": (c_i32, [P(c_u32), c_i32, c_i32, P(ct_measure_opts), P(c_f32)]),
     "ct_probe_copy": (c_i32, [P(c_u32), c_i32, ctypes.c_void_p, ctypes.c_void_p, c_i64, P(ct_measure_opts),
@@ -352,6 +367,46 @@ def ct_cross_eval(op, scheds: Sequence, masks: Sequence, opts: ct_measure_opts, 
     _check(lib().ct_cross_eval(ctypes.byref(o), arr, len(scheds), _arr(mk, c_u32), len(masks), MASK_WORDS,
                                ctypes.byref(opts), _ptr(x), _ptr(w), _ptr(y), _arr(M, c_f32)))
     return M.reshape(len(scheds), len(masks))
+
+
+def make_search_opts(seed=0, batch=16, budget=256, patience=0, sa_chains=32, sa_steps=100, explore=0.25,
+                     eps=0.01, sa_temp=0.5) -> ct_search_opts:
+    return ct_search_opts(int(seed), int(batch), int(budget), int(patience), int(sa_chains), int(sa_steps),
+                          float(explore), float(eps), float(sa_temp))
+
+
+def ct_search_propose(op, measured: Sequence, lat_us, status, so: ct_search_opts, round_: int,
+                      cap: Optional[int] = None) -> List[ct_schedule]:
+    n = len(measured)
+    cap = so.batch if cap is None else cap
+    arr = schedule_array(measured) if n else None
+    lat = np.ascontiguousarray(lat_us, dtype=np.float32) if n else np.zeros(1, np.float32)
+    st = np.ascontiguousarray(status, dtype=np.int32) if n else np.zeros(1, np.int32)
+    out = (ct_schedule * max(cap, 1))()
+    cnt = c_i32()
+    o = make_op(op)
+    _check(lib().ct_search_propose(ctypes.byref(o), arr, _arr(lat, c_f32), _arr(st, c_i32), n, ctypes.byref(so),
+                                   int(round_), out, int(cap), ctypes.byref(cnt)))
+    return [out[i] for i in range(cnt.value)]
+
+
+def ct_search(op, so: ct_search_opts, cu_mask, stage1: ct_measure_opts, stage2: ct_measure_opts, top_t: int,
+              eps: float, x, w, y):
+    """Guided search on one mask: (measured schedules, stage-1 latencies,
+    statuses, result fields as a dict)."""
+    n = so.budget
+    meas = (ct_schedule * n)()
+    lat = np.zeros(n, dtype=np.float32)
+    st = np.zeros(n, dtype=np.int32)
+    res = ct_search_result()
+    o = make_op(op)
+    m = mask_array(cu_mask) if cu_mask is not None else None
+    _check(lib().ct_search(ctypes.byref(o), ctypes.byref(so), m, MASK_WORDS if m is not None else 0,
+                           ctypes.byref(stage1), ctypes.byref(stage2), int(top_t), float(eps), _ptr(x), _ptr(w),
+                           _ptr(y), meas, _arr(lat, c_f32), _arr(st, c_i32), ctypes.byref(res)))
+    k = res.n_measured
+    info = {f: getattr(res, f) for f, _ in ct_search_result._fields_ if f != "pad_"}
+    return [meas[i] for i in range(k)], lat[:k], st[:k], info
 
 
 def ct_probe_cus(cu_mask, blocks: int = 4096) -> np.ndarray:
