@@ -243,30 +243,17 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
                                  "(%.2f TFLOP/s)." % (statistics.mean(red) / 1e3, len(red), both / 1e3,
                                                       replay["tflops"] * replay["latency_us"] / (both / 1e3)))
     if replay and fetch_dir and write_dir:
-        k = short_name(replay["kernel"])
-        f = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
-        w = counter_per_dispatch(write_dir, "WRITE_SIZE")
-        kf = [v for name, vs in f.items() if k in name for v in vs]
-        kw = [v for name, vs in w.items() if k in name for v in vs]
-        cf = [v for name, vs in f.items() if "copy_kernel" in name for v in vs]
-        cw = [v for name, vs in w.items() if "copy_kernel" in name for v in vs]
-        nbytes = replay.get("copy_bytes_each_way", 0)
-        if kf and kw and cf and cw and nbytes:
-            sf = nbytes / (max(cf) * 1024.0)
-            sw = nbytes / (max(cw) * 1024.0)
-            fetch = statistics.median(kf) * 1024.0 * sf
-            write = statistics.median(kw) * 1024.0 * sw
+        t = traffic_block(replay, fetch_dir, write_dir)
+        if t is not None:
             lines += ["", "## HBM traffic (counters)", "",
                       "| counter | copy kernel KiB (known %d MiB) | scale | kernel KiB per launch (median of %d) "
-                      "| kernel bytes per launch |" % (nbytes >> 20, len(kf)),
+                      "| kernel bytes per launch |" % (replay["copy_bytes_each_way"] >> 20, t["n"]),
                       "|---|---|---|---|---|",
-                      "| FETCH_SIZE | %.0f | %.4f | %.1f | %.0f |" % (max(cf), sf, statistics.median(kf), fetch),
-                      "| WRITE_SIZE | %.0f | %.4f | %.1f | %.0f |" % (max(cw), sw, statistics.median(kw), write)]
-            sched = replay["schedule"]
-            block = {"kernel": replay["kernel"], "layer": replay["layer"], "threads": sched.get("threads"),
-                     "blocks": sched.get("blocks"), "lds_bytes": sched.get("lds_bytes"),
-                     "knobs": sched.get("knobs"), "fetch_bytes": fetch, "write_bytes": write,
-                     "traffic_bytes": fetch + write, "source_hash": kernel_source_hash(replay["kernel"])}
+                      "| FETCH_SIZE | %.0f | %.4f | %.1f | %.0f |" % (t["copy_fetch_kib"], t["scale_f"], t["fetch_kib"],
+                                                                 t["block"]["fetch_bytes"]),
+                      "| WRITE_SIZE | %.0f | %.4f | %.1f | %.0f |" % (t["copy_write_kib"], t["scale_w"], t["write_kib"],
+                                                                 t["block"]["write_bytes"])]
+            block = t["block"]
         else:
             lines += ["", "Counter runs incomplete: traffic not derived."]
     if block:
@@ -274,39 +261,122 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
     return "\n".join(lines) + "\n"
 
 
+def _json_blocks(text: str):
+    """Every fenced json block of a summary, parsed (unparsable ones skipped)."""
+    pos = 0
+    while True:
+        start = text.find("```json\n", pos)
+        if start < 0:
+            return
+        end = text.find("```", start + 8)
+        if end < 0:
+            return
+        try:
+            yield json.loads(text[start + 8:end])
+        except ValueError:
+            pass
+        pos = end + 3
+
+
 def find_traffic(profiles_dir: str, kernel: str, shape: dict):
     """Traffic bytes per launch for `kernel` with this launch shape from a
     summary under profiles_dir, or None (no summary, another shape, or the
     kernel's sources changed since the counters were taken)."""
     want = kernel_source_hash(kernel)
+    if want is None:
+        return None
     for path in sorted(glob.glob(os.path.join(profiles_dir, "*.md"))):
-        text = open(path).read()
-        start = text.rfind("```json\n")
-        if start < 0:
-            continue
-        try:
-            blk = json.loads(text[start + 8:text.index("```", start + 8)])["traffic"]
-        except (ValueError, KeyError):
-            continue
-        if (blk.get("kernel") == kernel and blk.get("threads") == shape.get("threads")
-                and blk.get("blocks") == shape.get("blocks") and blk.get("knobs") == shape.get("knobs")
-                and want is not None and blk.get("source_hash") == want):
-            return blk
+        with open(path) as fh:
+            text = fh.read()
+        for doc in _json_blocks(text):
+            blk = doc.get("traffic") if isinstance(doc, dict) else None
+            if not isinstance(blk, dict):
+                continue
+            if (blk.get("kernel") == kernel and blk.get("threads") == shape.get("threads")
+                    and blk.get("blocks") == shape.get("blocks") and blk.get("knobs") == shape.get("knobs")
+                    and blk.get("source_hash") == want):
+                return blk
     return None
+
+
+def traffic_block(replay: dict, fetch_dir: str, write_dir: str):
+    """(FETCH, WRITE) medians in KiB, copy-kernel scales and the traffic block
+    of one replayed schedule, or None if a counter run is incomplete."""
+    k = short_name(replay["kernel"])
+    f = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
+    w = counter_per_dispatch(write_dir, "WRITE_SIZE")
+    kf = [v for name, vs in f.items() if k in name for v in vs]
+    kw = [v for name, vs in w.items() if k in name for v in vs]
+    cf = [v for name, vs in f.items() if "copy_kernel" in name for v in vs]
+    cw = [v for name, vs in w.items() if "copy_kernel" in name for v in vs]
+    nbytes = replay.get("copy_bytes_each_way", 0)
+    if not (kf and kw and cf and cw and nbytes):
+        return None
+    sf = nbytes / (max(cf) * 1024.0)
+    sw = nbytes / (max(cw) * 1024.0)
+    fetch = statistics.median(kf) * 1024.0 * sf
+    write = statistics.median(kw) * 1024.0 * sw
+    sched = replay["schedule"]
+    block = {"kernel": replay["kernel"], "layer": replay["layer"], "threads": sched.get("threads"),
+             "blocks": sched.get("blocks"), "lds_bytes": sched.get("lds_bytes"),
+             "knobs": sched.get("knobs"), "fetch_bytes": fetch, "write_bytes": write,
+             "traffic_bytes": fetch + write, "source_hash": kernel_source_hash(replay["kernel"])}
+    return {"fetch_kib": statistics.median(kf), "write_kib": statistics.median(kw), "n": len(kf),
+            "copy_fetch_kib": max(cf), "copy_write_kib": max(cw), "scale_f": sf, "scale_w": sw, "block": block}
+
+
+def traffic_table(entries, cmds=()) -> str:
+    """Summary of several replayed schedules' counter runs: one row and one
+    traffic block each. entries: (replay dict, fetch dir, write dir)."""
+    lines = ["# HBM traffic of candidate schedules (FETCH_SIZE / WRITE_SIZE counters)", "",
+             "Each schedule was replayed alone (back-to-back launches on slot 0 of its share) under one "
+             "counter per run; the copy kernel of the same run, over a buffer of known size, calibrates "
+             "the counters.", "", "Commands (one pair per schedule, `$ARG` = layer:family:knobs as listed):", ""]
+    lines += ["    " + c for c in cmds]
+    lines += ["", "| layer | kernel | knobs | launches | FETCH KiB | WRITE KiB | scale F / W | traffic bytes "
+              "| replay us |", "|---|---|---|---|---|---|---|---|---|"]
+    blocks = []
+    for rep, fdir, wdir in entries:
+        t = traffic_block(rep, fdir, wdir)
+        knobs = ",".join(str(v) for v in rep["schedule"]["knobs"].values())
+        if t is None:
+            lines.append("| %s | `%s` | %s | - | incomplete | | | | %.3f |" % (
+                rep["layer"], rep["kernel"], knobs, rep["latency_us"]))
+            continue
+        lines.append("| %s | `%s` | %s | %d | %.1f | %.1f | %.4f / %.4f | %.0f | %.3f |" % (
+            rep["layer"], rep["kernel"], knobs, t["n"], t["fetch_kib"], t["write_kib"], t["scale_f"], t["scale_w"],
+            t["block"]["traffic_bytes"], rep["latency_us"]))
+        blocks.append(t["block"])
+    for b in blocks:
+        lines += ["", "```json", json.dumps({"traffic": b}), "```"]
+    return "\n".join(lines) + "\n"
 
 
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
-    ap.add_argument("--trace", required=True)
+    ap.add_argument("--trace", default=None)
     ap.add_argument("--bench", default=None, help="file holding bench.py's JSON line")
     ap.add_argument("--replay", default=None, help="file holding tuner --replay's JSON line")
     ap.add_argument("--fetch", default=None)
     ap.add_argument("--write", default=None)
+    ap.add_argument("--entry", action="append", default=[], metavar="REPLAY_JSON:FETCH_DIR:WRITE_DIR",
+                    help="traffic-table mode: one replayed schedule and its two counter runs")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args(argv)
-    text = summarize(a.trace, _read_json_line(a.bench, '"metric"'), _read_json_line(a.replay, '"kernel"'),
-                     a.fetch, a.write, a.cmd)
+    if a.entry:
+        entries = []
+        for e in a.entry:
+            rj, fd, wd = e.split(":")
+            rep = _read_json_line(rj, '"kernel"')
+            if rep is not None:
+                entries.append((rep, fd, wd))
+        text = traffic_table(entries, a.cmd)
+    else:
+        if not a.trace:
+            ap.error("--trace is required without --entry")
+        text = summarize(a.trace, _read_json_line(a.bench, '"metric"'), _read_json_line(a.replay, '"kernel"'),
+                         a.fetch, a.write, a.cmd)
     if a.out:
         with open(a.out, "w") as fh:
             fh.write(text)

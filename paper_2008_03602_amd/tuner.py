@@ -84,6 +84,9 @@ class JobResult:
                                if np.any(self.status1 == k)},
              "winner_pos": self.winner_pos, "winner_lat_us": self.winner_lat_us,
              "t_start": self.t_start, "t_end": self.t_end}
+        d["top"] = [{"pos": int(p), "lat2_us": float(l), "family": int(self.candidates[int(p)].family),
+                     "knobs": list(describe_schedule(self.op, self.candidates[int(p)])["knobs"].values())}
+                    for p, l in zip(self.top_pos, self.lat2)]
         if s is not None:
             d["winner"] = describe_schedule(self.op, s)
             d["winner_tflops"] = self.op.flops() / (self.winner_lat_us * 1e-6) / 1e12
