@@ -45,7 +45,7 @@ namespace ct {
 
 constexpr int kHaloSlots = 16;  // halo loads per wave per chunk (max)
 constexpr int kFiltSlots = 16;  // filter loads per wave per chunk (max)
-constexpr int kRegCopies = 4;   // register-staged 16-byte copies of each kind per wave (max)
+constexpr int kRegCopies = 8;   // register-staged 16-byte copies of each kind per wave (max)
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct IgF32Args {
@@ -331,12 +331,13 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   };
 
-  // STAGES = 2 with 16-byte copies and at most kRegCopies of each kind per
-  // wave: the next chunk goes through registers instead (16-byte loads that
-  // stay in flight during the MFMAs, stored to LDS after them). A copy
+  // With 16-byte copies and at most kRegCopies of each kind per wave, chunks
+  // go through registers instead: 16-byte loads, then LDS stores. A copy
   // straight to LDS holds its wave about one L2 round trip on this device,
-  // so several of them in a row stall the wave that should be issuing MFMAs.
-  const bool via_regs = STAGES == 2 && a.vec_h && a.vec_f && a.n_halo <= kRegCopies &&
+  // so several in a row serialise, while plain loads are all in flight at
+  // once. With STAGES = 2 the next chunk's loads stay in flight during the
+  // current chunk's MFMAs and are stored to LDS after them.
+  const bool via_regs = a.vec_h && a.vec_f && a.n_halo <= kRegCopies &&
                         ((a.n_filt_units + nw - 1) >> a.lg_nw) <= kRegCopies;
   f32x4 rh[kRegCopies], rf[kRegCopies];
   auto load_regs = [&](int ch) {
@@ -360,7 +361,15 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       if (j < n_filt_w && f_lane) *(f32x4*)(as + f_dst[j] + lane * 4) = rf[j];
   };
 
-  if constexpr (STAGES == 1) {
+  if (STAGES == 1 && via_regs) {
+    for (int ch = ch_begin; ch < ch_end; ++ch) {
+      load_regs(ch);
+      store_regs(0);
+      __syncthreads();
+      compute(0);
+      __syncthreads();  // the next chunk's stores overwrite this stage
+    }
+  } else if constexpr (STAGES == 1) {
     for (int ch = ch_begin; ch < ch_end; ++ch) {
       issue(ch, 0);
       wait_copies();
@@ -370,8 +379,8 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   } else if (via_regs) {
     if (ch_begin < ch_end) {
-      issue(ch_begin, 0);
-      wait_copies();
+      load_regs(ch_begin);
+      store_regs(0);
     }
     __syncthreads();
     for (int ch = ch_begin; ch < ch_end; ++ch) {
@@ -453,7 +462,10 @@ IgF32Fn igf32_pick_spec(int spec) {
 }
 template <int MF, int TM, int TN>
 IgF32Fn igf32_pick_stages(int stages, int spec) {
-  return stages == 2 ? igf32_pick_spec<MF, TM, TN, 2>(spec) : igf32_pick_spec<MF, TM, TN, 1>(spec);
+  if constexpr (TM * TN * MfmaF32<MF>::ACC > 128)
+    return nullptr;  // accumulator tiles the validator rejects: not instantiated
+  else
+    return stages == 2 ? igf32_pick_spec<MF, TM, TN, 2>(spec) : igf32_pick_spec<MF, TM, TN, 1>(spec);
 }
 template <int MF, int TM>
 IgF32Fn igf32_pick_tn(int tn, int stages, int spec) {
