@@ -14,13 +14,20 @@
 //
 // Compile-time: MK, MW, LDS, UNR and the filter/stride specialisation
 // (generic, 1x1 s1/s2, 3x3 pad 1 s1/s2). Runtime: tiles, CT, SPLIT.
-// Every global access is bounds-checked against the tensor extents.
+// Global reads are raw buffer loads with 32-bit offsets: an element outside
+// the tensor (padding, a tile past the edge) gets an offset past the buffer,
+// which the hardware reads as 0. A load then needs one offset register and no
+// branch, so a thread keeps many in flight: with few threads per CU (small
+// grids) this, not the arithmetic, sets the time. The staging of an LDS chunk
+// issues kStageBatch loads per thread before the first LDS store.
 #include <hip/hip_runtime.h>
 
 #include "ct_internal.h"
 #include "k_util.h"
 
 namespace ct {
+
+constexpr int kStageBatch = 16;  // staging loads in flight per thread
 
 struct DirectArgs {
   int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
@@ -35,11 +42,15 @@ struct DirectArgs {
   int64_t ny;
 };
 
+// Threads per block that leave registers for an MK x MW accumulator tile
+// and its operands without spilling.
+__host__ __device__ constexpr int direct_max_threads(int tile) { return tile >= 16 ? 512 : 1024; }
+
 __host__ __device__ constexpr int spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
 __host__ __device__ constexpr int spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
 
 template <int MK, int MW, bool LDS, int SPEC, int UNR>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(direct_max_threads(MK * MW))
 direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ out,
                   DirectArgs a) {
   constexpr int RC = spec_r(SPEC), STC = spec_stride(SPEC);
@@ -71,6 +82,9 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
   const int c_end = min(C, c_begin + a.cps * a.ct);
   const int ih_org = oh0 * sh - ph, iw_org = ow0 * sw - pw;
   const float* xn = x + (int64_t)n * C * H * W;
+  const int HW = H * W;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(xn, (int64_t)C * HW * 4);
+  const __amdgpu_buffer_rsrc_t rwt = make_rsrc(w, (int64_t)K * C * RS * 4);
 
   for (int cc = c_begin; cc < c_end; cc += a.ct) {
     const int nc = min(a.ct, c_end - cc);
@@ -79,41 +93,48 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
       float* wsm = smem + a.ct * a.ih_t * a.iw_t;
       const int plane = a.ih_t * a.iw_t;
       const int xt = a.ct * plane;
-      // Stage the halo tile and the filter chunk four elements per thread at a
-      // time: four branch-free loads, then four LDS stores.
-      for (int e0 = t; e0 < xt; e0 += 4 * a.threads) {
-        float v[4];
+      // Stage the halo tile and the filter chunk: batches of kStageBatch
+      // loads per thread while the wave's first lane (its lowest element)
+      // needs a whole batch, then batches of four. Every load is issued
+      // before the batch's first LDS store; an element past the tile or
+      // outside the tensor reads 0 through the buffer's range check.
+      auto stage = [&](const int total, const __amdgpu_buffer_rsrc_t r, auto byte_off, float* dst) {
+        int e0 = t;
+        for (; e0 < total && __builtin_amdgcn_readfirstlane(e0) + (kStageBatch - 1) * a.threads < total;
+             e0 += kStageBatch * a.threads) {
+          float v[kStageBatch];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e = e0 + u * a.threads;
-          const int c = qdiv(e, a.inv_plane);
-          const int rem = e - c * plane;
-          const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
-          const int gh = ih_org + hh, gw = iw_org + ww;
-          const bool ok = e < xt && c < nc && gh >= 0 && gh < H && gw >= 0 && gw < W;
-          v[u] = load_or_zero(xn, ((int64_t)(cc + c) * H + gh) * W + gw, ok);
+          for (int u = 0; u < kStageBatch; ++u) v[u] = bload1(r, byte_off(e0 + u * a.threads));
+#pragma unroll
+          for (int u = 0; u < kStageBatch; ++u)
+            if (e0 + u * a.threads < total) dst[e0 + u * a.threads] = v[u];
         }
+        for (; e0 < total; e0 += 4 * a.threads) {
+          float v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (e0 + u * a.threads < xt) xs[e0 + u * a.threads] = v[u];
-      }
+          for (int u = 0; u < 4; ++u) v[u] = bload1(r, byte_off(e0 + u * a.threads));
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (e0 + u * a.threads < total) dst[e0 + u * a.threads] = v[u];
+        }
+      };
+      stage(xt, rx, [&](const int e) {
+        const int c = qdiv(e, a.inv_plane);
+        const int rem = e - c * plane;
+        const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
+        const int gh = ih_org + hh, gw = iw_org + ww;
+        const bool ok = e < xt && c < nc && (unsigned)gh < (unsigned)H && (unsigned)gw < (unsigned)W;
+        return ok ? ((cc + c) * HW + gh * W + gw) * 4 : kOob;
+      }, xs);
       const int crs = a.ct * RS;
       const int wt = a.tk * crs;
-      for (int e0 = t; e0 < wt; e0 += 4 * a.threads) {
-        float v[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e = e0 + u * a.threads;
-          const int kk = qdiv(e, a.inv_crs);
-          const int rem = e - kk * crs;
-          const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
-          const bool ok = e < wt && k0 + kk < K && c < nc;
-          v[u] = load_or_zero(w, ((int64_t)(k0 + kk) * C + cc + c) * RS + rs, ok);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (e0 + u * a.threads < wt) wsm[e0 + u * a.threads] = v[u];
-      }
+      stage(wt, rwt, [&](const int e) {
+        const int kk = qdiv(e, a.inv_crs);
+        const int rem = e - kk * crs;
+        const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
+        const bool ok = e < wt && k0 + kk < K && c < nc;
+        return ok ? (((k0 + kk) * C + cc + c) * RS + rs) * 4 : kOob;
+      }, wsm);
       __syncthreads();
 #pragma unroll UNR
       for (int c = 0; c < nc; ++c) {
@@ -145,21 +166,21 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
         // K-1 (its sums are never stored)
         const float* wrow[MK];
 #pragma unroll
-        for (int i = 0; i < MK; ++i) wrow[i] = w + (int64_t)min(kb + i, K - 1) * C * RS;
+        for (int i = 0; i < MK; ++i) wrow[i] = w + min(kb + i, K - 1) * C * RS;
 #pragma unroll UNR
         for (int c = 0; c < nc; ++c) {
-          const float* xc = xn + (int64_t)(cc + c) * H * W;
+          const int xo = (cc + c) * HW;
           const int co = (cc + c) * RS;
           for (int r = 0; r < R; ++r) {
             const int gh = oh * sh - ph + r * dh;
-            const bool hok = gh >= 0 && gh < H && oh < a.OH;
+            const bool hok = (unsigned)gh < (unsigned)H && oh < a.OH;
             for (int s = 0; s < S; ++s) {
               float xv[MW], wv[MK];
 #pragma unroll
               for (int j = 0; j < MW; ++j) {
                 const int ow = ow0 + lc + j * a.cols;
                 const int gw = ow * sw - pw + s * dw;
-                xv[j] = load_or_zero(xc, (int64_t)gh * W + gw, hok && gw >= 0 && gw < W);
+                xv[j] = bload1(rx, hok && (unsigned)gw < (unsigned)W ? (xo + gh * W + gw) * 4 : kOob);
               }
 #pragma unroll
               for (int i = 0; i < MK; ++i) wv[i] = wrow[i][co + r * S + s];

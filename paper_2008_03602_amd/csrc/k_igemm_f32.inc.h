@@ -97,11 +97,6 @@ struct MfmaF32<16> {
   __device__ static int row(int e, int lane) { return 4 * (lane >> 4) + e; }
 };
 
-constexpr int kOob = 0x7FFFFFF0;  // byte offset beyond every buffer: reads as 0
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
 // 16 bytes at byte offset off of r (0 past the buffer's range)
 __device__ __forceinline__ f32x4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));

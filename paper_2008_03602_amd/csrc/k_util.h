@@ -14,6 +14,19 @@ __device__ __forceinline__ T load_or_zero(const T* __restrict__ p, int64_t idx, 
   return ok ? v : T{};
 }
 
+// Raw buffer resource over `bytes` bytes at base: loads at byte offsets at or
+// past `bytes` return 0 (the hardware range check), so an out-of-range
+// element needs no branch and no clamped address.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+constexpr int kOob = 0x7FFFFFF0;  // byte offset beyond every buffer: reads as 0
+
+// One word at byte offset off of r (0 past the buffer's range).
+__device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
 // floor(n / d) for 0 <= n < 2^22 given inv = 1/d in fp32: (n + 1/2)/d lies at
 // least 1/(2d) from an integer and the fp32 product errs by less than that.
 __device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }

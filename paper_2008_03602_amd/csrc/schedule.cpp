@@ -189,8 +189,13 @@ static int geom_direct(const OpX& x, const ct_schedule& s, Geom* g, std::string*
   if (tow > fit(f.knobs[TOW], x.ow)) REJECT("tow exceeds the output width");
   if (tk > fit(f.knobs[TK], o.k)) REJECT("tk exceeds K");
   if (ctile > fit(f.knobs[CT], x.cg)) REJECT("ct exceeds C");
+  if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
+    REJECT("tensor too large for 32-bit buffer offsets");
   const int64_t threads = (int64_t)(tk / mk) * (toh * tow / mw);
   if (threads < kMinThreads || threads > kMaxThreads) REJECT("threads per block out of range");
+  // the register budget of the kernel's launch bounds: an accumulator tile of
+  // 16 or more outputs per thread allows at most 512 threads
+  if (mk * mw >= 16 && threads > 512) REJECT("too many threads for the accumulator tile");
   const int64_t chunks = cdiv(x.cg, ctile);
   int64_t cps = 0;
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty channel range");
