@@ -22,6 +22,8 @@
 // issues kStageBatch loads per thread before the first LDS store.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "ct_internal.h"
 #include "k_util.h"
 
@@ -86,13 +88,97 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(xn, (int64_t)C * HW * 4);
   const __amdgpu_buffer_rsrc_t rwt = make_rsrc(w, (int64_t)K * C * RS * 4);
 
-  for (int cc = c_begin; cc < c_end; cc += a.ct) {
+  // LDS path: the block's MACs over nc staged channels
+  auto compute_lds = [&](const int nc) {
+    const float* xs = smem;
+    const float* wsm = smem + a.ct * a.ih_t * a.iw_t;
+    const int plane = a.ih_t * a.iw_t;
+#pragma unroll UNR
+    for (int c = 0; c < nc; ++c) {
+      const float* xr = xs + c * plane + (lr * sh) * a.iw_t + lc * sw;
+      const float* wr = wsm + (tki * MK * a.ct + c) * RS;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          float xv[MW], wv[MK];
+#pragma unroll
+          for (int j = 0; j < MW; ++j) xv[j] = xr[(r * dh) * a.iw_t + j * a.cols * sw + s * dw];
+#pragma unroll
+          for (int i = 0; i < MK; ++i) wv[i] = wr[i * a.ct * RS + r * S + s];
+#pragma unroll
+          for (int i = 0; i < MK; ++i)
+#pragma unroll
+            for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+        }
+      }
+    }
+  };
+  // byte offsets of staging element e of the chunk starting at channel cc
+  // (nc channels): halo element, then filter element; kOob outside
+  const int plane = a.ih_t * a.iw_t;
+  const int xt = a.ct * plane;
+  const int crs = a.ct * RS;
+  const int wt = a.tk * crs;
+  auto x_off = [&](const int e, const int cc, const int nc) {
+    const int c = qdiv(e, a.inv_plane);
+    const int rem = e - c * plane;
+    const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
+    const int gh = ih_org + hh, gw = iw_org + ww;
+    const bool ok = e < xt && c < nc && (unsigned)gh < (unsigned)H && (unsigned)gw < (unsigned)W;
+    return ok ? ((cc + c) * HW + gh * W + gw) * 4 : kOob;
+  };
+  auto w_off = [&](const int e, const int cc, const int nc) {
+    const int kk = qdiv(e, a.inv_crs);
+    const int rem = e - kk * crs;
+    const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
+    const bool ok = e < wt && k0 + kk < K && c < nc;
+    return ok ? (((k0 + kk) * C + cc + c) * RS + rs) * 4 : kOob;
+  };
+  // Chunks small enough for NS staging elements per thread go through
+  // registers: the next chunk's loads are in flight during this chunk's
+  // MACs, so a block pays one memory round trip per chunk only once.
+  auto prefetched = [&](auto ns) {
+    constexpr int NS = decltype(ns)::value;
+    float px[NS], pw[NS];
+    auto fetch = [&](const int cc) {
+      const int nc = min(a.ct, c_end - cc);
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        px[u] = bload1(rx, x_off(t + u * a.threads, cc, nc));
+        pw[u] = bload1(rwt, w_off(t + u * a.threads, cc, nc));
+      }
+    };
+    float* xs = smem;
+    float* wsm = smem + xt;
+    if (c_begin < c_end) fetch(c_begin);
+    for (int cc = c_begin; cc < c_end; cc += a.ct) {
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        const int e = t + u * a.threads;
+        if (e < xt) xs[e] = px[u];
+        if (e < wt) wsm[e] = pw[u];
+      }
+      __syncthreads();
+      if (cc + a.ct < c_end) fetch(cc + a.ct);
+      compute_lds(min(a.ct, c_end - cc));
+      __syncthreads();  // the next chunk's stores overwrite the tiles
+    }
+  };
+  const int n_stage = (max(xt, wt) + a.threads - 1) / a.threads;
+  bool done = false;
+  if constexpr (LDS && MK * MW < 8) {  // registers to spare beside the accumulators
+    done = true;
+    if (n_stage <= 1) prefetched(std::integral_constant<int, 1>{});
+    else if (n_stage <= 2) prefetched(std::integral_constant<int, 2>{});
+    else done = false;
+  }
+
+  for (int cc = c_begin; cc < c_end && !done; cc += a.ct) {
     const int nc = min(a.ct, c_end - cc);
     if constexpr (LDS) {
       float* xs = smem;
-      float* wsm = smem + a.ct * a.ih_t * a.iw_t;
-      const int plane = a.ih_t * a.iw_t;
-      const int xt = a.ct * plane;
+      float* wsm = smem + xt;
       // Stage the halo tile and the filter chunk: batches of kStageBatch
       // loads per thread while the wave's first lane (its lowest element)
       // needs a whole batch, then batches of four. Every load is issued
@@ -118,44 +204,10 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
             if (e0 + u * a.threads < total) dst[e0 + u * a.threads] = v[u];
         }
       };
-      stage(xt, rx, [&](const int e) {
-        const int c = qdiv(e, a.inv_plane);
-        const int rem = e - c * plane;
-        const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
-        const int gh = ih_org + hh, gw = iw_org + ww;
-        const bool ok = e < xt && c < nc && (unsigned)gh < (unsigned)H && (unsigned)gw < (unsigned)W;
-        return ok ? ((cc + c) * HW + gh * W + gw) * 4 : kOob;
-      }, xs);
-      const int crs = a.ct * RS;
-      const int wt = a.tk * crs;
-      stage(wt, rwt, [&](const int e) {
-        const int kk = qdiv(e, a.inv_crs);
-        const int rem = e - kk * crs;
-        const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
-        const bool ok = e < wt && k0 + kk < K && c < nc;
-        return ok ? (((k0 + kk) * C + cc + c) * RS + rs) * 4 : kOob;
-      }, wsm);
+      stage(xt, rx, [&](const int e) { return x_off(e, cc, nc); }, xs);
+      stage(wt, rwt, [&](const int e) { return w_off(e, cc, nc); }, wsm);
       __syncthreads();
-#pragma unroll UNR
-      for (int c = 0; c < nc; ++c) {
-        const float* xr = xs + c * plane + (lr * sh) * a.iw_t + lc * sw;
-        const float* wr = wsm + (tki * MK * a.ct + c) * RS;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-#pragma unroll
-          for (int s = 0; s < S; ++s) {
-            float xv[MW], wv[MK];
-#pragma unroll
-            for (int j = 0; j < MW; ++j) xv[j] = xr[(r * dh) * a.iw_t + j * a.cols * sw + s * dw];
-#pragma unroll
-            for (int i = 0; i < MK; ++i) wv[i] = wr[i * a.ct * RS + r * S + s];
-#pragma unroll
-            for (int i = 0; i < MK; ++i)
-#pragma unroll
-              for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
-          }
-        }
-      }
+      compute_lds(nc);
       __syncthreads();
     } else {
       // kb: first output channel of this thread. When every wave lies inside
