@@ -170,12 +170,21 @@ int ct_kernel_name(const ct_op *op, const ct_schedule *s, char *buf, int cap);
  * of each applicable family's valid grid indices in ascending order. Writes
  * up to cap schedules of it in that order; *count = its full size. */
 int ct_valid_space(const ct_op *op, ct_schedule *out, int64_t cap, int64_t *count);
-/* Seeded sample of n candidates without replacement: a partial Fisher-Yates
- * shuffle of the candidate space driven by splitmix64 from state
+/* Seeded sample of n candidates without replacement, stratified by kernel
+ * family (a family is a schedule template, which a TVM-style tuner tunes as a
+ * task of its own). The valid space (ct_valid_space order: family by family,
+ * grid order within) is split by family; family f gets a quota q_f: equal
+ * shares of min(n, |V|), the remainder to the first families, and a family
+ * with fewer valid schedules than its share hands the rest on, in rounds,
+ * until the total is reached. Within family f, a partial Fisher-Yates shuffle
+ * of its schedules driven by splitmix64 from state
  *   seed ^ (0x9E3779B97F4A7C15 * (1 + config_id)) ^ (0xC0FFEE << 32) ^ layer_id
- * (first output discarded): for i < n, j = i + next() mod (|V| - i), swap.
+ *        ^ (0xD1B54A32D192ED03 * family)
+ * (first output discarded): for i < q_f, j = i + next() mod (|V_f| - i), swap.
+ * out[] interleaves the families: the k-th pick of each family in family
+ * order, then the (k+1)-th, so every prefix of the list is balanced.
  * out[i] is the candidate at sample position i. If |V| < n, all |V| are
- * returned (in shuffled order). *n_out = number written. */
+ * returned. *n_out = number written. */
 int ct_sample(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_id,
               int32_t n, ct_schedule *out, int32_t *n_out);
 

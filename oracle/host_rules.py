@@ -4,11 +4,17 @@ Plain Python, written from the stated definitions, sharing nothing with the
 library. Each function names the rule it follows.
 
 * Candidate selection with no history is random (paper, section 2.1, stage
-  "select configurations"). The rule fixed here: a partial Fisher-Yates
-  shuffle of the ascending valid candidate list, driven by splitmix64
-  (Steele, Lea, Flood, OOPSLA 2014), from state
-  seed ^ (GAMMA * (1 + config_id) mod 2^64) ^ (0xC0FFEE << 32) ^ layer_id,
-  first output discarded; j = i + next() mod (|V| - i).
+  "select configurations"), per schedule template (kernel family), since a
+  TVM-style tuner tunes each template as a task of its own. The rule fixed
+  here: the ascending valid list is split by family; family quotas are equal
+  shares of min(n, |V|), the remainder going to the first families, and a
+  family smaller than its share hands the rest on, in rounds; within a family
+  a partial Fisher-Yates shuffle driven by splitmix64 (Steele, Lea, Flood,
+  OOPSLA 2014) from state
+  seed ^ (GAMMA * (1 + config_id) mod 2^64) ^ (0xC0FFEE << 32) ^ layer_id
+       ^ (0xD1B54A32D192ED03 * family mod 2^64),
+  first output discarded, j = i + next() mod (|V_f| - i); the output takes
+  the k-th pick of every family in family order, then the (k+1)-th.
 * A configuration's latency is the median of its repeats (the profile stage
   measures execution time; the statistic is this build's reading).
 * The best configuration is the one with the lowest latency (implied by the
@@ -43,21 +49,52 @@ class SplitMix64:
         return z ^ (z >> 31)
 
 
-def sampler_state(seed: int, config_id: int, layer_id: int) -> int:
+def sampler_state(seed: int, config_id: int, layer_id: int, family: int) -> int:
     return (seed ^ ((GAMMA * (1 + config_id)) & MASK64) ^ ((0xC0FFEE << 32) & MASK64)
-            ^ (layer_id & 0xFFFFFFFF)) & MASK64
+            ^ (layer_id & 0xFFFFFFFF) ^ ((0xD1B54A32D192ED03 * family) & MASK64)) & MASK64
 
 
-def sample_positions(space_size: int, n: int, seed: int, config_id: int, layer_id: int) -> List[int]:
-    """Indices into the ascending valid list, in sample order (partial Fisher-Yates)."""
-    rng = SplitMix64(sampler_state(seed, config_id, layer_id))
+def partial_shuffle(size: int, take: int, state: int) -> List[int]:
+    """The first `take` positions of a Fisher-Yates shuffle of range(size)."""
+    rng = SplitMix64(state)
     rng.next()  # the first output is discarded
-    v = list(range(space_size))
+    v = list(range(size))
     out = []
-    for i in range(min(n, space_size)):
-        j = i + rng.next() % (space_size - i)
+    for i in range(min(take, size)):
+        j = i + rng.next() % (size - i)
         v[i], v[j] = v[j], v[i]
         out.append(v[i])
+    return out
+
+
+def family_quotas(sizes: Sequence[int], n: int) -> List[int]:
+    """Equal shares of min(n, total), the remainder to the first families; a
+    family smaller than its share hands the rest on, round after round."""
+    q = [0] * len(sizes)
+    rem = min(n, sum(sizes))
+    while rem > 0:
+        act = [f for f in range(len(sizes)) if q[f] < sizes[f]]
+        base, extra = divmod(rem, len(act))
+        for i, f in enumerate(act):
+            add = min(base + (1 if i < extra else 0), sizes[f] - q[f])
+            q[f] += add
+            rem -= add
+    return q
+
+
+def sample_positions(families: Sequence[int], sizes: Sequence[int], n: int, seed: int, config_id: int,
+                     layer_id: int) -> List[int]:
+    """Indices into the ascending valid list (families in order, family f
+    holding sizes[f] entries), in sample order."""
+    q = family_quotas(sizes, n)
+    starts = [sum(sizes[:f]) for f in range(len(sizes))]
+    picks = [partial_shuffle(sizes[f], q[f], sampler_state(seed, config_id, layer_id, families[f]))
+             for f in range(len(sizes))]
+    out = []
+    for k in range(max(q, default=0)):
+        for f in range(len(sizes)):
+            if k < q[f]:
+                out.append(starts[f] + picks[f][k])
     return out
 
 

@@ -600,17 +600,53 @@ int ct_sample(const ct_op* op, uint64_t seed, int32_t config_id, int32_t layer_i
   std::vector<ct_schedule> v;
   int rc = valid_space(op, &v);
   if (rc) return rc;
-  uint64_t state = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)(1 + (int64_t)config_id)) ^
-                   (0xC0FFEEull << 32) ^ (uint64_t)(uint32_t)layer_id;
-  splitmix64_next(&state);  // the first output is discarded
-  const uint64_t size = v.size();
-  const uint64_t take = std::min<uint64_t>((uint64_t)n, size);
-  for (uint64_t i = 0; i < take; ++i) {
-    const uint64_t j = i + splitmix64_next(&state) % (size - i);
-    std::swap(v[i], v[j]);
-    out[i] = v[i];
+  // the space is family by family: [begin, end) of each family present
+  std::vector<size_t> fb, fe;
+  for (size_t i = 0; i < v.size(); ++i) {
+    if (i == 0 || v[i].family != v[i - 1].family) {
+      if (i) fe.push_back(i);
+      fb.push_back(i);
+    }
   }
-  *n_out = (int32_t)take;
+  if (!v.empty()) fe.push_back(v.size());
+  const size_t nf = fb.size();
+  // quotas: equal shares, the remainder to the first families, a family's
+  // unused share handed on until n is reached or every family is exhausted
+  std::vector<uint64_t> q(nf, 0);
+  uint64_t rem = std::min<uint64_t>((uint64_t)n, v.size());
+  while (rem > 0) {
+    std::vector<size_t> act;
+    for (size_t f = 0; f < nf; ++f)
+      if (q[f] < fe[f] - fb[f]) act.push_back(f);
+    const uint64_t base = rem / act.size(), extra = rem % act.size();
+    for (size_t i = 0; i < act.size(); ++i) {
+      const size_t f = act[i];
+      const uint64_t add = std::min<uint64_t>(base + (i < extra ? 1 : 0), (fe[f] - fb[f]) - q[f]);
+      q[f] += add;
+      rem -= add;
+    }
+  }
+  // per family: partial Fisher-Yates of its part of the space
+  const uint64_t state0 = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)(1 + (int64_t)config_id)) ^
+                          (0xC0FFEEull << 32) ^ (uint64_t)(uint32_t)layer_id;
+  std::vector<std::vector<ct_schedule>> picks(nf);
+  for (size_t f = 0; f < nf; ++f) {
+    uint64_t state = state0 ^ (0xD1B54A32D192ED03ull * (uint64_t)v[fb[f]].family);
+    splitmix64_next(&state);  // the first output is discarded
+    const uint64_t size = fe[f] - fb[f];
+    ct_schedule* part = v.data() + fb[f];
+    for (uint64_t i = 0; i < q[f]; ++i) {
+      const uint64_t j = i + splitmix64_next(&state) % (size - i);
+      std::swap(part[i], part[j]);
+      picks[f].push_back(part[i]);
+    }
+  }
+  // interleaved: the k-th pick of every family in family order, then k + 1
+  int32_t m = 0;
+  for (uint64_t k = 0; m < (int32_t)std::min<uint64_t>((uint64_t)n, v.size()); ++k)
+    for (size_t f = 0; f < nf; ++f)
+      if (k < q[f]) out[m++] = picks[f][k];
+  *n_out = m;
   return CT_OK;
 }
 

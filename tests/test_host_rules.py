@@ -62,12 +62,30 @@ def test_sampler_is_bit_identical_to_oracle(cfg, layer):
     c = W.config(cfg)
     op = c.ops[layer]
     space = L.ct_valid_space(op)
+    fams = sorted({s.family for s in space})
+    sizes = [sum(1 for s in space if s.family == f) for f in fams]
     for seed in (0, 1, 12345):
         got = L.ct_sample(op, seed, cfg, layer, c.n_candidates)
-        pos = HR.sample_positions(len(space), c.n_candidates, seed, cfg, layer)
+        pos = HR.sample_positions(fams, sizes, c.n_candidates, seed, cfg, layer)
         assert len(got) == len(pos) == min(c.n_candidates, len(space))
         assert [L.schedule_tuple(s) for s in got] == [L.schedule_tuple(space[p]) for p in pos]
         assert len(set(pos)) == len(pos)
+
+
+def test_family_quotas_by_hand():
+    assert HR.family_quotas([5, 100], 20) == [5, 15]      # a small family hands its share on
+    assert HR.family_quotas([3, 3], 10) == [3, 3]         # the whole space
+    assert HR.family_quotas([10, 10, 10], 10) == [4, 3, 3]
+    assert HR.family_quotas([1, 2, 50], 9) == [1, 2, 6]
+    assert HR.family_quotas([], 5) == []
+
+
+def test_sample_is_balanced_and_interleaved_across_families():
+    op = W.config(2).ops[1]  # direct and fp32 MFMA families both apply
+    got = L.ct_sample(op, 0, 2, 1, 256)
+    fams = [s.family for s in got]
+    assert fams.count(1) == fams.count(4) == 128
+    assert fams[:6] == [1, 4, 1, 4, 1, 4]
 
 
 def test_sampler_determinism_and_seed_sensitivity():
