@@ -45,7 +45,7 @@ namespace ct {
 
 constexpr int kHaloSlots = 16;  // halo loads per wave per chunk (max)
 constexpr int kFiltSlots = 16;  // filter loads per wave per chunk (max)
-constexpr int kRegCopies = 8;   // register-staged 16-byte copies of each kind per wave (max)
+constexpr int kRegCopies = 4;   // register-staged 16-byte copies of each kind per wave (max)
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 struct IgF32Args {
@@ -326,13 +326,14 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   };
 
-  // With 16-byte copies and at most kRegCopies of each kind per wave, chunks
-  // go through registers instead: 16-byte loads, then LDS stores. A copy
+  // STAGES = 2 with 16-byte copies and at most kRegCopies of each kind per
+  // wave: the next chunk goes through registers instead (16-byte loads that
+  // stay in flight during the MFMAs, stored to LDS after them). A copy
   // straight to LDS holds its wave about one L2 round trip on this device,
-  // so several in a row serialise, while plain loads are all in flight at
-  // once. With STAGES = 2 the next chunk's loads stay in flight during the
-  // current chunk's MFMAs and are stored to LDS after them.
-  const bool via_regs = a.vec_h && a.vec_f && a.n_halo <= kRegCopies &&
+  // so several of them in a row stall the wave that should be issuing MFMAs.
+  // (Measured: staging the single-stage chunks, or the first chunk, the same
+  // way is a few percent slower than copying them straight to LDS.)
+  const bool via_regs = STAGES == 2 && a.vec_h && a.vec_f && a.n_halo <= kRegCopies &&
                         ((a.n_filt_units + nw - 1) >> a.lg_nw) <= kRegCopies;
   f32x4 rh[kRegCopies], rf[kRegCopies];
   auto load_regs = [&](int ch) {
@@ -356,15 +357,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       if (j < n_filt_w && f_lane) *(f32x4*)(as + f_dst[j] + lane * 4) = rf[j];
   };
 
-  if (STAGES == 1 && via_regs) {
-    for (int ch = ch_begin; ch < ch_end; ++ch) {
-      load_regs(ch);
-      store_regs(0);
-      __syncthreads();
-      compute(0);
-      __syncthreads();  // the next chunk's stores overwrite this stage
-    }
-  } else if constexpr (STAGES == 1) {
+  if constexpr (STAGES == 1) {
     for (int ch = ch_begin; ch < ch_end; ++ch) {
       issue(ch, 0);
       wait_copies();
@@ -374,8 +367,8 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   } else if (via_regs) {
     if (ch_begin < ch_end) {
-      load_regs(ch_begin);
-      store_regs(0);
+      issue(ch_begin, 0);
+      wait_copies();
     }
     __syncthreads();
     for (int ch = ch_begin; ch < ch_end; ++ch) {
