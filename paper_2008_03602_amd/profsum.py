@@ -331,21 +331,21 @@ def traffic_table(entries, cmds=()) -> str:
     lines = ["# HBM traffic of candidate schedules (FETCH_SIZE / WRITE_SIZE counters)", "",
              "Each schedule was replayed alone (back-to-back launches on slot 0 of its share) under one "
              "counter per run; the copy kernel of the same run, over a buffer of known size, calibrates "
-             "the counters.", "", "Commands (one pair per schedule, `$ARG` = layer:family:knobs as listed):", ""]
+             "the counters. (Kernel times under counter collection are not representative and are not "
+             "listed.)", "", "Commands (one pair per schedule, `$ARG` = layer:family:knobs as listed):", ""]
     lines += ["    " + c for c in cmds]
-    lines += ["", "| layer | kernel | knobs | launches | FETCH KiB | WRITE KiB | scale F / W | traffic bytes "
-              "| replay us |", "|---|---|---|---|---|---|---|---|---|"]
+    lines += ["", "| layer | kernel | knobs | launches | FETCH KiB | WRITE KiB | scale F / W | traffic bytes |",
+              "|---|---|---|---|---|---|---|---|"]
     blocks = []
     for rep, fdir, wdir in entries:
         t = traffic_block(rep, fdir, wdir)
         knobs = ",".join(str(v) for v in rep["schedule"]["knobs"].values())
         if t is None:
-            lines.append("| %s | `%s` | %s | - | incomplete | | | | %.3f |" % (
-                rep["layer"], rep["kernel"], knobs, rep["latency_us"]))
+            lines.append("| %s | `%s` | %s | - | incomplete | | | |" % (rep["layer"], rep["kernel"], knobs))
             continue
-        lines.append("| %s | `%s` | %s | %d | %.1f | %.1f | %.4f / %.4f | %.0f | %.3f |" % (
+        lines.append("| %s | `%s` | %s | %d | %.1f | %.1f | %.4f / %.4f | %.0f |" % (
             rep["layer"], rep["kernel"], knobs, t["n"], t["fetch_kib"], t["write_kib"], t["scale_f"], t["scale_w"],
-            t["block"]["traffic_bytes"], rep["latency_us"]))
+            t["block"]["traffic_bytes"]))
         blocks.append(t["block"])
     for b in blocks:
         lines += ["", "```json", json.dumps({"traffic": b}), "```"]

@@ -143,3 +143,48 @@ def test_every_family_covered_on_config1_shape():
         yd.fill_(float("nan"))
         L.conv2d_run(op, s, xd, wd, yd)
         check_close(op, yd.cpu().numpy(), ref, a, "config1 " + sched_str(s), split=4)
+
+
+def _direct_class(op, s):
+    """Which staging path a direct schedule takes (mirrors the kernel's choice)."""
+    toh, tow, tk, mk, mw, lds, ct = (s.knob[i] for i in range(7))
+    cols = tow // mw
+    threads = (tk // mk) * toh * cols
+    if not lds:
+        return "regs-uniform-w" if (toh * cols) % 64 == 0 else "regs"
+    ih = (toh - 1) * op.stride_h + (op.r - 1) * op.dil_h + 1
+    iw = (tow - 1) * op.stride_w + (op.s - 1) * op.dil_w + 1
+    xt, wt = ct * ih * iw, tk * ct * op.r * op.s
+    n_stage = (max(xt, wt) + threads - 1) // threads
+    if mk * mw < 8 and n_stage <= 2:
+        return "prefetch-%d" % n_stage
+    return "batch16" if n_stage >= 16 else "batch4"
+
+
+@pytest.mark.parametrize("op", [W.conv("deep3x3", 1, 48, 9, 72, 3, 1), F32_OPS[1], F32_OPS[5]],
+                         ids=lambda o: o.name)
+def test_direct_staging_paths_match_oracle(op):
+    # every way the direct family reads its operands: registers with vector or
+    # scalar filter loads, LDS chunks through registers (one or two elements
+    # per thread), and LDS staging in batches of four or sixteen loads
+    x, w = make_inputs(op, "uniform", seed=31)
+    ref, a = reference(op, x, w)
+    xd, wd, yd = to_device(op, x, w)
+    by = {}
+    for s in L.ct_valid_space(op):
+        if s.family == W.FAM_DIRECT_F32:
+            by.setdefault(_direct_class(op, s), []).append(s)
+    rng = random.Random(5)
+    seen = set()
+    for cls in sorted(by):
+        for s in rng.sample(by[cls], min(3, len(by[cls]))):
+            tag = "%s %s [%s]" % (op.name, sched_str(s), cls)
+            note(tag)
+            yd.fill_(float("nan"))
+            L.conv2d_run(op, s, xd, wd, yd)
+            split = L.ct_launch_shape(op, s)["kernels"]
+            check_close(op, yd.cpu().numpy(), ref, a, tag, split=4 if split > 1 else 1)
+            seen.add(cls)
+    print(op.name, "paths:", sorted(seen))
+    if op.name == "deep3x3":
+        assert {"regs", "prefetch-1", "prefetch-2", "batch4", "batch16"} <= seen

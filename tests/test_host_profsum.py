@@ -1,0 +1,71 @@
+"""Host-side profile summaries: counter calibration, traffic table and the
+lookup bench.py uses (synthetic counter files; no profiler needed)."""
+import csv
+import json
+import os
+
+import pytest
+
+from paper_2008_03602_amd import profsum
+
+KNAME = "void ct::igemm_f32_kernel<16, 1, 1, 1, 3>(float const*, float const*, float*, ct::IgF32Args)"
+
+
+def _pmc(dirpath, counter, rows):
+    os.makedirs(dirpath, exist_ok=True)
+    with open(os.path.join(dirpath, "x_counter_collection.csv"), "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for i, (name, v) in enumerate(rows):
+            w.writerow([i + 1, name, counter, v])
+
+
+def _replay(knobs, nbytes=1 << 30):
+    return {"layer": "r18.2", "kernel": "igemm_f32_kernel<16, 1, 1, 1, 3>",
+            "schedule": {"threads": 512, "blocks": 224, "lds_bytes": 25856, "knobs": knobs},
+            "latency_us": 9.0, "copy_bytes_each_way": nbytes}
+
+
+def test_traffic_is_scaled_by_the_copy_kernel(tmp_path):
+    # the copy kernel of 1 GiB reads as 524288 KiB FETCH (scale 2) and 1048576 KiB WRITE (scale 1)
+    f, w = str(tmp_path / "f"), str(tmp_path / "w")
+    _pmc(f, "FETCH_SIZE", [(KNAME, 3000.0), (KNAME, 3100.0), (KNAME, 3050.0), ("ct::copy_kernel(...)", 524288.0)])
+    _pmc(w, "WRITE_SIZE", [(KNAME, 784.0)] * 3 + [("ct::copy_kernel(...)", 1048576.0)])
+    t = profsum.traffic_block(_replay({"mfma": 16}), f, w)
+    assert t["scale_f"] == pytest.approx(2.0) and t["scale_w"] == pytest.approx(1.0)
+    assert t["block"]["fetch_bytes"] == pytest.approx(3050.0 * 1024 * 2)   # median of the three
+    assert t["block"]["write_bytes"] == pytest.approx(784.0 * 1024)
+    assert t["block"]["traffic_bytes"] == pytest.approx(3050.0 * 2048 + 784.0 * 1024)
+
+
+def test_incomplete_counter_runs_give_no_traffic(tmp_path):
+    f, w = str(tmp_path / "f"), str(tmp_path / "w")
+    _pmc(f, "FETCH_SIZE", [(KNAME, 3000.0)])  # no copy kernel in the run
+    _pmc(w, "WRITE_SIZE", [(KNAME, 784.0), ("ct::copy_kernel(...)", 1048576.0)])
+    assert profsum.traffic_block(_replay({"mfma": 16}), f, w) is None
+
+
+def test_table_lookup_matches_kernel_shape_knobs_and_source_hash(tmp_path):
+    entries = []
+    for i, knobs in enumerate(({"mfma": 16, "cpc": 16}, {"mfma": 16, "cpc": 32})):
+        f, w = str(tmp_path / ("f%d" % i)), str(tmp_path / ("w%d" % i))
+        _pmc(f, "FETCH_SIZE", [(KNAME, 1000.0 * (i + 1)), ("ct::copy_kernel(...)", 524288.0)])
+        _pmc(w, "WRITE_SIZE", [(KNAME, 784.0), ("ct::copy_kernel(...)", 1048576.0)])
+        entries.append((_replay(knobs), f, w))
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "table.md").write_text(profsum.traffic_table(entries, ["cmd"]))
+    shape = {"threads": 512, "blocks": 224, "knobs": {"mfma": 16, "cpc": 32}}
+    blk = profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 1, 1, 3>", shape)
+    assert blk is not None and blk["fetch_bytes"] == pytest.approx(2000.0 * 2048)
+    # another shape, other knobs or another kernel: no figure
+    assert profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 1, 1, 3>",
+                                dict(shape, blocks=448)) is None
+    assert profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 1, 1, 3>",
+                                dict(shape, knobs={"mfma": 16, "cpc": 8})) is None
+    assert profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 2, 1, 3>", shape) is None
+    # a block whose source hash differs from the current sources is stale
+    text = (prof / "table.md").read_text()
+    h = profsum.kernel_source_hash("igemm_f32_kernel<16, 1, 1, 1, 3>")
+    (prof / "table.md").write_text(text.replace(h, "0" * 16))
+    assert profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 1, 1, 3>", shape) is None
