@@ -1,5 +1,6 @@
 """Benchmark: one step = one full pass of the tuning hot path on the ResNet-18
-batch-1 conv set (12 layers, fp32 NCHW, 256 seeded candidates per layer):
+batch-1 conv set (12 layers, fp32 NCHW, 256 seeded candidates per layer,
+128 from each of the two kernel families that apply: direct and fp32 MFMA):
 
   1. tune every layer at 25% of the CUs, as 4 concurrent clients on the 4
      disjoint 64-CU slots, which take the layers from one shared queue,
@@ -161,7 +162,8 @@ def main() -> int:
         "value": value, "unit": "candidates/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": elapsed / a.steps * 1e3, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "ResNet-18 b1 conv set (12 layers) fp32 NCHW, %d seeded candidates per layer, "
+        "config": {"workload": "ResNet-18 b1 conv set (12 layers) fp32 NCHW, %d seeded candidates per layer "
+                               "(equal shares per kernel family), "
                                "tuned at 25/50/100%% CUs by 4/2/1 concurrent CU-masked clients sharing a "
                                "largest-first layer queue, then a 3x3 cross-evaluation of the winners" % cfg.n_candidates,
                    "candidates_per_step": n_per_step, "layers": len(layers), "seed": cfg.seed,
