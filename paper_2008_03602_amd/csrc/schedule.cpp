@@ -54,7 +54,7 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"wn", 3, {1, 2, 4}},
       {"ws", 3, {1, 2, 4}},
       {"tpw", 4, {8, 16, 32, 64}},
-      {"cpc", 6, {1, 2, 4, 8, 16, 32}},
+      {"cpc", 7, {1, 2, 4, 8, 16, 32, 64}},
       {"stages", 2, {1, 2}},
       {"split", 4, {1, 2, 4, 8}}}},
 };
