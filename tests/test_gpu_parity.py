@@ -188,3 +188,33 @@ def test_direct_staging_paths_match_oracle(op):
     print(op.name, "paths:", sorted(seen))
     if op.name == "deep3x3":
         assert {"regs", "prefetch-1", "prefetch-2", "batch4", "batch16"} <= seen
+
+
+# Degenerate shapes: a one-pixel image (only the centre tap of a padded 3x3
+# filter sees data), a filter as large as the image (one output pixel),
+# one input and one output channel, a stride larger than the filter, a batch
+# of three, and a one-row bf16 image.
+DEGENERATE_OPS = [
+    W.conv("one_pixel", 1, 8, 1, 8, 3, 1),
+    W.Op("filter_covers_image", 1, 5, 7, 7, 6, 7, 7, 1, 1, 0, 0, 1, 1, 1, 0, 0),
+    W.conv("one_channel", 2, 1, 9, 1, 3, 1),
+    W.conv("stride3_1x1", 1, 12, 10, 8, 1, 3, 0),
+    W.conv("batch3", 3, 16, 6, 16, 3, 1),
+    W.Op("pwbf_one_row", 2, 16, 1, 9, 24, 1, 1, 1, 1, 0, 0, 1, 1, 1, W.DT_BF16, W.LAYOUT_NHWC),
+]
+
+
+@pytest.mark.parametrize("op", DEGENERATE_OPS, ids=lambda o: o.name)
+def test_degenerate_shapes_match_oracle(op):
+    fams = _run_sample(op, 12, seed=11)
+    assert fams, op.name
+    # every family that has a schedule for the shape, including the MFMA ones
+    space_fams = {s.family for s in L.ct_valid_space(op)}
+    for fam in sorted(space_fams - fams):
+        _run_sample(op, 4, seed=12, family=fam)
+
+
+@pytest.mark.parametrize("op", DEGENERATE_OPS, ids=lambda o: o.name)
+def test_degenerate_shapes_bit_exact_on_integers(op):
+    bf16 = op.dtype == W.DT_BF16
+    _run_sample(op, 8, seed=13, dist="int", int_range=8 if bf16 else 2, exact=True)

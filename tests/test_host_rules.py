@@ -171,3 +171,20 @@ def test_xcd_swizzle_is_a_bijection():
 def test_median_rule():
     assert HR.median([3, 1, 2]) == 2
     assert HR.median([4, 1, 2, 3]) == np.float32(2.5)
+
+
+def test_degenerate_ops_are_refused_at_the_boundary():
+    """An op with no work (zero batch, an output with no pixels) or an
+    impossible grouping is an argument error, not an empty candidate list."""
+    some = L.ct_sample(W.conv("ok", 1, 4, 8, 8, 3, 1), 0, 0, 0, 1)[0]
+    bad = [W.Op("n0", 0, 4, 8, 8, 4, 3, 3, 1, 1, 1, 1, 1, 1, 1, 0, 0),
+           W.Op("c0", 1, 0, 8, 8, 4, 3, 3, 1, 1, 1, 1, 1, 1, 1, 0, 0),
+           W.Op("no_output", 1, 4, 2, 2, 4, 5, 5, 1, 1, 0, 0, 1, 1, 1, 0, 0),
+           W.Op("stride0", 1, 4, 8, 8, 4, 3, 3, 0, 1, 1, 1, 1, 1, 1, 0, 0),
+           W.Op("groups", 1, 6, 8, 8, 4, 3, 3, 1, 1, 1, 1, 1, 1, 4, 0, 0)]
+    for op in bad:
+        with pytest.raises(L.CtError) as e:
+            L.ct_validate(op, some)
+        assert e.value.code == -1, op.name
+        with pytest.raises(L.CtError):
+            L.ct_valid_space(op)
