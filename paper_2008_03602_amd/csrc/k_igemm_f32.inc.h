@@ -460,7 +460,8 @@ IgF32Fn igf32_pick_tn(int tn, int stages, int spec) {
   switch (tn) {
     case 1: return igf32_pick_stages<MF, TM, 1>(stages, spec);
     case 2: return igf32_pick_stages<MF, TM, 2>(stages, spec);
-    default: return igf32_pick_stages<MF, TM, 4>(stages, spec);
+    case 4: return igf32_pick_stages<MF, TM, 4>(stages, spec);
+    default: return igf32_pick_stages<MF, TM, 7>(stages, spec);
   }
 }
 

@@ -46,14 +46,16 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"lds", 2, {0, 1}},
       {"split", 3, {1, 2, 4}},
       {"swizzle", 2, {0, 1}}}},
+    // tn 7 and the tile widths 7..56 give pixel tiles of whole rows of the
+    // 7*2^k-wide maps of these networks (two 56-pixel rows = 7 MFMA tiles)
     {CT_FAM_IGEMM_F32, "igemm_mfma_f32", f32g_knob::COUNT,
      {{"mfma", 2, {16, 32}},
       {"tm", 3, {1, 2, 4}},
-      {"tn", 3, {1, 2, 4}},
+      {"tn", 4, {1, 2, 4, 7}},
       {"wm", 3, {1, 2, 4}},
       {"wn", 3, {1, 2, 4}},
       {"ws", 3, {1, 2, 4}},
-      {"tpw", 4, {8, 16, 32, 64}},
+      {"tpw", 8, {7, 8, 14, 16, 28, 32, 56, 64}},
       {"cpc", 7, {1, 2, 4, 8, 16, 32, 64}},
       {"stages", 2, {1, 2}},
       {"split", 4, {1, 2, 4, 8}}}},
