@@ -297,6 +297,9 @@ typedef struct ct_search_opts {
     float eps;           /* relative improvement that resets the patience count       */
     float sa_temp;       /* starting temperature, in units of log latency; it falls   */
                          /* linearly to 0 over a chain                                 */
+    int32_t cus;         /* CUs of the share being tuned, for the cost model's grid   */
+                         /* features; 0 = ct_search counts the mask (all 256 for      */
+                         /* ct_search_propose)                                        */
 } ct_search_opts;
 
 typedef struct ct_search_result {

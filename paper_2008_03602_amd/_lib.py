@@ -68,7 +68,7 @@ class ct_client(ctypes.Structure):
 
 class ct_search_opts(ctypes.Structure):
     _fields_ = [("seed", c_u64), ("batch", c_i32), ("budget", c_i32), ("patience", c_i32), ("sa_chains", c_i32),
-                ("sa_steps", c_i32), ("explore", c_f32), ("eps", c_f32), ("sa_temp", c_f32)]
+                ("sa_steps", c_i32), ("explore", c_f32), ("eps", c_f32), ("sa_temp", c_f32), ("cus", c_i32)]
 
 
 class ct_search_result(ctypes.Structure):
@@ -370,9 +370,9 @@ def ct_cross_eval(op, scheds: Sequence, masks: Sequence, opts: ct_measure_opts, 
 
 
 def make_search_opts(seed=0, batch=16, budget=256, patience=0, sa_chains=32, sa_steps=100, explore=0.25,
-                     eps=0.01, sa_temp=0.5) -> ct_search_opts:
+                     eps=0.01, sa_temp=0.5, cus=0) -> ct_search_opts:
     return ct_search_opts(int(seed), int(batch), int(budget), int(patience), int(sa_chains), int(sa_steps),
-                          float(explore), float(eps), float(sa_temp))
+                          float(explore), float(eps), float(sa_temp), int(cus))
 
 
 def ct_search_propose(op, measured: Sequence, lat_us, status, so: ct_search_opts, round_: int,

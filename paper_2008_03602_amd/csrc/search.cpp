@@ -7,8 +7,9 @@
 //
 // The cost model is this library's own, not the paper's gradient-boosted
 // trees: per kernel family, ridge regression of log latency on a one-hot
-// code of every knob value plus launch-geometry features (grid size, block
-// size, LDS bytes), which carry the knob interactions that matter most.
+// code of every knob value plus launch-geometry features (grid size against
+// the CUs of the share being tuned, block size, LDS bytes, padded work),
+// which carry the knob interactions that matter most.
 // Everything here is host code and deterministic for a given seed and given
 // measurements.
 #include <algorithm>
@@ -27,7 +28,7 @@
 namespace ct {
 namespace {
 
-constexpr int kGeomFeatures = 5;
+constexpr int kGeomFeatures = 7;
 constexpr double kRidge = 0.3;
 
 struct Space {
@@ -87,8 +88,28 @@ int feature_count(const FamilyDef& f) {
   return n;
 }
 
-// Features of a valid schedule (false if it does not validate).
-bool features(const OpX& x, const ct_schedule& s, std::vector<double>* out) {
+// Output elements the grid of a schedule computes, padding included (the
+// tiles times their sizes): against the op's own output volume this is the
+// work a tile shape wastes on ragged edges.
+double padded_outputs(const OpX& x, const ct_schedule& s, const Geom& g) {
+  const ct_op& o = x.op;
+  switch (s.family) {
+    case CT_FAM_DIRECT_F32:
+      return (double)(g.tiles_h * s.knob[direct_knob::TOH]) * (double)(g.tiles_w * s.knob[direct_knob::TOW]) *
+             (double)(g.tiles_k * s.knob[direct_knob::TK]) * (double)o.n;
+    case CT_FAM_DEPTHWISE_F32:
+      return (double)(g.tiles_h * s.knob[dw_knob::TOH]) * (double)(g.tiles_w * s.knob[dw_knob::TOW]) *
+             (double)(g.tiles_c * s.knob[dw_knob::TC]) * (double)(g.tiles_n * s.knob[dw_knob::NB]);
+    case CT_FAM_IGEMM_BF16:
+      return (double)(g.tiles_h * g.bm) * (double)(g.tiles_k * g.bn);
+    default:
+      return (double)o.n * (double)(g.tiles_h * g.tph) * (double)(g.tiles_w * g.tpw) * (double)(g.tiles_k * g.bm);
+  }
+}
+
+// Features of a valid schedule on a share of `cus` CUs (false if it does not
+// validate).
+bool features(const OpX& x, const ct_schedule& s, int cus, std::vector<double>* out) {
   const FamilyDef& f = *family_def(s.family);
   Geom g;
   if (compute_geom(x, s, &g, nullptr) != CT_OK) return false;
@@ -102,11 +123,15 @@ bool features(const OpX& x, const ct_schedule& s, std::vector<double>* out) {
   }
   const double lb = std::log2((double)std::max<int64_t>(g.blocks, 1));
   const double waves = std::log2((double)std::max<int64_t>(g.blocks * ((g.threads + 63) / 64), 1));
+  const double bpc = (double)std::max<int64_t>(g.blocks, 1) / (double)std::max(cus, 1);  // blocks per CU
   (*out)[o + 0] = lb;
-  (*out)[o + 1] = (lb - 8.0) * (lb - 8.0) / 8.0;  // distance from one block per CU
+  (*out)[o + 1] = std::log2(bpc) * std::log2(bpc) / 8.0;  // distance from one block per CU of the share
   (*out)[o + 2] = std::log2((double)std::max(g.threads, 1));
   (*out)[o + 3] = g.lds_bytes / 65536.0;
   (*out)[o + 4] = waves;
+  // the last round of blocks: ceil(bpc) rounds for bpc rounds of work
+  (*out)[o + 5] = std::log2(std::ceil(bpc) / bpc);
+  (*out)[o + 6] = std::log2(std::max(padded_outputs(x, s, g) / (double)x.ny, 1.0));  // padded work
   return true;
 }
 
@@ -146,7 +171,7 @@ struct Model {
   struct Fam { bool fitted = false; double mean = 0.0; std::vector<double> beta; };
   Fam fam[CT_NUM_FAMILIES + 1];
 
-  void fit(const OpX& x, const ct_schedule* s, const float* lat, const int32_t* st, int n) {
+  void fit(const OpX& x, int cus, const ct_schedule* s, const float* lat, const int32_t* st, int n) {
     double sum = 0.0;
     int cnt = 0;
     for (int i = 0; i < n; ++i)
@@ -161,7 +186,7 @@ struct Model {
       std::vector<double> feat;
       for (int i = 0; i < n; ++i) {
         if (s[i].family != f || st[i] != CT_S_OK || !std::isfinite(lat[i]) || !(lat[i] > 0.0f)) continue;
-        if (!features(x, s[i], &feat)) continue;
+        if (!features(x, s[i], cus, &feat)) continue;
         X.push_back(feat);
         y.push_back(std::log((double)lat[i]));
       }
@@ -186,10 +211,10 @@ struct Model {
   }
 
   // Predicted log latency of a valid schedule.
-  double predict(const OpX& x, const ct_schedule& s, std::vector<double>* feat) const {
+  double predict(const OpX& x, int cus, const ct_schedule& s, std::vector<double>* feat) const {
     const Fam& m = fam[s.family];
     if (!m.fitted) return any ? global_mean : 0.0;
-    if (!features(x, s, feat)) return INFINITY;
+    if (!features(x, s, cus, feat)) return INFINITY;
     double p = m.mean;
     for (size_t i = 0; i < feat->size(); ++i) p += (*feat)[i] * m.beta[i];
     return p;
@@ -248,7 +273,8 @@ int propose(const Space& sp, const ct_schedule* meas, const float* lat, const in
   std::unordered_set<uint64_t> chosen;
 
   Model model;
-  model.fit(sp.x, meas, lat, st, n);
+  const int cus = so.cus > 0 ? so.cus : 256;
+  model.fit(sp.x, cus, meas, lat, st, n);
   int n_model = 0;
   if (model.any) {
     n_model = want - (int)std::floor(so.explore * want + 0.5);
@@ -274,11 +300,11 @@ int propose(const Space& sp, const ct_schedule* meas, const float* lat, const in
       const std::vector<int>& best = ok[(size_t)c % nf];
       ct_schedule s = (c < chains / 2 && !best.empty()) ? meas[best[((size_t)c / nf) % best.size()]]
                                                          : draw(sp, (uint64_t)c, &rng);
-      double e = model.predict(sp.x, s, &feat);
+      double e = model.predict(sp.x, cus, s, &feat);
       for (int t = 0; t < steps; ++t) {
         const double temp = so.sa_temp * (1.0 - (double)t / steps);
         const ct_schedule c2 = neighbour(sp.x, s, &rng);
-        const double e2 = model.predict(sp.x, c2, &feat);
+        const double e2 = model.predict(sp.x, cus, c2, &feat);
         if (e2 <= e || (temp > 0.0 && uniform01(&rng) < std::exp(-(e2 - e) / temp))) {
           s = c2;
           e = e2;
@@ -328,7 +354,7 @@ int propose(const Space& sp, const ct_schedule* meas, const float* lat, const in
 
 bool opts_ok(const ct_search_opts* so) {
   return so && so->batch > 0 && so->budget > 0 && so->patience >= 0 && so->sa_chains >= 0 && so->sa_steps >= 0 &&
-         so->explore >= 0.0f && so->explore <= 1.0f && so->eps >= 0.0f && so->sa_temp >= 0.0f;
+         so->explore >= 0.0f && so->explore <= 1.0f && so->eps >= 0.0f && so->sa_temp >= 0.0f && so->cus >= 0;
 }
 
 double now_s() {
@@ -375,12 +401,19 @@ int ct_search(const ct_op* op, const ct_search_opts* so, const uint32_t* cu_mask
   int rc = build_space(*op, &sp);
   if (rc) return rc;
   const bool progress = std::getenv("CT_PROGRESS") != nullptr;
+  // the cost model scores grids against the CUs of the share being tuned
+  ct_search_opts sopt = *so;
+  if (sopt.cus == 0) {
+    int c = 0;
+    for (int i = 0; cu_mask && i < words; ++i) c += __builtin_popcount(cu_mask[i]);
+    sopt.cus = c > 0 ? c : 256;
+  }
   int n = 0, since = 0;
   double best = INFINITY;
   while (n < so->budget) {
     const int want = std::min(so->batch, so->budget - n);
     double t0 = now_s();
-    const int got = propose(sp, measured, lat_us, status, n, *so, res->rounds, measured + n, want);
+    const int got = propose(sp, measured, lat_us, status, n, sopt, res->rounds, measured + n, want);
     double t1 = now_s();
     res->propose_s += t1 - t0;
     if (got == 0) break;
