@@ -86,7 +86,8 @@ struct MfmaF32<32> {
   static constexpr int ACC = 16, KSTEP = 2;
   typedef float V __attribute__((ext_vector_type(16)));
   __device__ static V op(float a, float b, V c) { return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0); }
-  // row of accumulator element e held by `lane` (column = lane % 32)
+  // row of accumulator element e held by `lane` (column = lane % 32); for both
+  // shapes it splits as row(e, 0) + row(0, lane)
   __device__ static int row(int e, int lane) { return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3); }
 };
 template <>
@@ -391,17 +392,28 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   }
 
   if (a.wsp > 1) {
-    // add the reduction groups' partial tiles in group order
+    // add the reduction groups' partial tiles in group order; a lane's
+    // accumulators of one MFMA tile sit side by side in LDS, so they move
+    // 16 bytes per access (the 64 lanes of a wave cover 64 consecutive
+    // 16-byte slots: no bank conflicts)
     __syncthreads();
-    float* red = smem;
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    f4* red = (f4*)smem;
+    constexpr int Q = ACC / 4;  // 16-byte quads per accumulator tile
     if (wg > 0) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int e = 0; e < ACC; ++e)
-            red[((((wg - 1) * wpg + wi) * TM * TN + i * TN + j) * ACC + e) * 64 + lane] = acc[i][j][e];
+          for (int qd = 0; qd < Q; ++qd) {
+            f4 v;
+            v.x = acc[i][j][4 * qd];
+            v.y = acc[i][j][4 * qd + 1];
+            v.z = acc[i][j][4 * qd + 2];
+            v.w = acc[i][j][4 * qd + 3];
+            red[((((wg - 1) * wpg + wi) * TM * TN + i * TN + j) * Q + qd) * 64 + lane] = v;
+          }
     }
     __syncthreads();
     if (wg > 0) return;
@@ -411,27 +423,59 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int e = 0; e < ACC; ++e)
-            acc[i][j][e] += red[((((g - 1) * wpg + wi) * TM * TN + i * TN + j) * ACC + e) * 64 + lane];
+          for (int qd = 0; qd < Q; ++qd) {
+            const f4 v = red[((((g - 1) * wpg + wi) * TM * TN + i * TN + j) * Q + qd) * 64 + lane];
+            acc[i][j][4 * qd] += v.x;
+            acc[i][j][4 * qd + 1] += v.y;
+            acc[i][j][4 * qd + 2] += v.z;
+            acc[i][j][4 * qd + 3] += v.w;
+          }
     }
   }
 
-  float* o = out + (int64_t)sp * a.ny;
+  // Store. An accumulator's output channel splits into a wave-uniform part
+  // (tile i, element e) and a lane part, so where the wave's whole channel
+  // tile exists each store is a buffer store whose scalar offset carries the
+  // uniform channel row and whose one 32-bit lane offset (channel-group row
+  // and pixel) is computed once per pixel column: no per-store address
+  // arithmetic on the vector ALU. A ragged channel tail checks every element.
   const int ohw = a.OH * a.OW;
+  const int kw = k0 + m_off;  // first output channel of this wave's tile
+  float* ob = out + (int64_t)sp * a.ny + (int64_t)(nimg * a.K + kw) * ohw;
+  if (kw + TM * MF <= a.K) {
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(ob, (int64_t)TM * MF * ohw * 4);
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int q = n_off + j * MF + lrow;
-    const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
-    const int oh = oh0 + pr, ow = ow0 + pc;
-    if (oh >= a.OH || ow >= a.OW) continue;
-    const int base = (nimg * a.K + k0 + m_off) * ohw + oh * a.OW + ow;  // y offset of channel k0+m_off
+    for (int j = 0; j < TN; ++j) {
+      const int q = n_off + j * MF + lrow;
+      const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
+      const int oh = oh0 + pr, ow = ow0 + pc;
+      if (oh >= a.OH || ow >= a.OW) continue;
+      const int lo = (M::row(0, lane) * ohw + oh * a.OW + ow) * 4;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < ACC; ++e) {
-        const int kr = i * MF + M::row(e, lane);
-        if (k0 + m_off + kr < a.K) o[base + kr * ohw] = acc[i][j][e];
-      }
+        for (int e = 0; e < ACC; ++e) {
+          // the element goes through a scalar first: a bit cast applied to a
+          // vector element directly has compiled to a read of element 0
+          const float v = acc[i][j][e];
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, lo, (i * MF + M::row(e, 0)) * ohw * 4, 0);
+        }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int q = n_off + j * MF + lrow;
+      const int pr = qdiv(q, a.inv_tpw), pc = q - pr * a.tpw;
+      const int oh = oh0 + pr, ow = ow0 + pc;
+      if (oh >= a.OH || ow >= a.OW) continue;
+      const int lo = oh * a.OW + ow;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < ACC; ++e) {
+          const int kr = i * MF + M::row(e, lane);
+          if (kw + kr < a.K) ob[(int64_t)kr * ohw + lo] = acc[i][j][e];
+        }
     }
   }
 }
