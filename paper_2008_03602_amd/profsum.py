@@ -167,7 +167,14 @@ def _read_json_line(path: str, key: str):
     return None
 
 
-def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None, cmds=()) -> str:
+def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None, cmds=(), traced_bench=None) -> str:
+    """Kernel table of a trace; with `bench` (bench.py's JSON line) the trace
+    durations of the kernel and launch shape it names, set beside its HIP-event
+    latency. `traced_bench` is the line the traced run itself printed, when
+    `bench` comes from an untraced run of the same command: the tracer adds
+    time to every launch, which reorders near-equal candidates, so the two
+    runs can name different winners; every candidate is screened on every
+    share in both, so the untraced winner's launches are in the trace."""
     tr = Trace(trace_dir)
     lines = ["# rocprofv3 kernel summary", ""]
     if tr.db is None and not tr.rows:
@@ -190,9 +197,20 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
         grid = blocks * threads if blocks and threads else None
         durs = tr.durations(kname, threads, grid, shape.get("lds_bytes"))
         lines += ["", "## Roofline kernel", "",
-                  "bench.py names `%s` (layer %s, %s blocks x %s threads, LDS %s bytes), %.3f GFLOP per launch."
-                  % (kname, rf.get("layer"), blocks, threads, shape.get("lds_bytes"),
+                  "bench.py%s names `%s` (layer %s, %s blocks x %s threads, LDS %s bytes, knobs %s), "
+                  "%.3f GFLOP per launch."
+                  % (" (untraced run)" if traced_bench else "", kname, rf.get("layer"), blocks, threads,
+                     shape.get("lds_bytes"), ",".join(str(v) for v in shape.get("knobs", {}).values()),
                      rf.get("flops_per_launch", 0) / 1e9), ""]
+        if traced_bench and "roofline" in traced_bench:
+            tr_rf = traced_bench["roofline"]
+            tr_sh = tr_rf.get("launch_shape", {})
+            same = tr_rf.get("kernel") == kname and tr_sh.get("knobs") == shape.get("knobs")
+            lines += ["The traced run of the same command named %s (%.3f us by its HIP events, which hold "
+                      "the tracer's per-launch cost); the rows below are the untraced winner's launches in "
+                      "the trace." % ("the same schedule" if same else "`%s` knobs %s" % (
+                          tr_rf.get("kernel"), ",".join(str(v) for v in tr_sh.get("knobs", {}).values())),
+                          tr_rf.get("latency_us", 0.0)), ""]
         if durs:
             avg = statistics.mean(durs) / 1e3
             groups = tr.by_stream(kname, threads, grid, shape.get("lds_bytes"))
@@ -219,8 +237,9 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
                           rf["flops_per_launch"] / (avg * 1e-6) / 1e12,
                           100.0 * rf["flops_per_launch"] / (avg * 1e-6) / 1e12 / rf["peak"], rf["peak"],
                           rf.get("unit", ""))]
-            lines.append("(The bench's first launch of each repeat follows a host-side event record, so "
-                         "its HIP-event mean also holds launch gaps that the trace does not.)")
+            if rf.get("latency_us", 0.0) > avg:
+                lines.append("(The bench's first launch of each repeat follows a host-side event record, so "
+                             "its HIP-event mean also holds launch gaps that the trace does not.)")
         else:
             lines.append("No dispatch of that kernel with that shape is in the trace.")
     if replay:
@@ -356,6 +375,8 @@ def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", default=None)
     ap.add_argument("--bench", default=None, help="file holding bench.py's JSON line")
+    ap.add_argument("--traced-bench", default=None,
+                    help="file holding the JSON line of the traced run, when --bench is an untraced run")
     ap.add_argument("--replay", default=None, help="file holding tuner --replay's JSON line")
     ap.add_argument("--fetch", default=None)
     ap.add_argument("--write", default=None)
@@ -376,7 +397,7 @@ def main(argv=None) -> int:
         if not a.trace:
             ap.error("--trace is required without --entry")
         text = summarize(a.trace, _read_json_line(a.bench, '"metric"'), _read_json_line(a.replay, '"kernel"'),
-                         a.fetch, a.write, a.cmd)
+                         a.fetch, a.write, a.cmd, _read_json_line(a.traced_bench, '"metric"'))
     if a.out:
         with open(a.out, "w") as fh:
             fh.write(text)
