@@ -241,18 +241,42 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
     }
   }
 
-  float* o = out + (int64_t)sp * a.ny;
+  // Store. An accumulator's pixel row is a wave-uniform part (tile i,
+  // element e) plus a lane part, so where every pixel row of the wave tile
+  // exists each store is a buffer store whose scalar offset carries the
+  // uniform row and whose one 32-bit lane offset (row group and channel) is
+  // computed once per channel column; a ragged pixel tail checks every
+  // element.
+  const int mw = m0 + m_off;  // first pixel row of this wave's tile
+  float* ob = out + (int64_t)sp * a.ny + (int64_t)mw * a.K;
+  if (mw + TM * MF <= a.npix) {
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(ob, (int64_t)TM * MF * a.K * 4);
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int n = n0 + n_off + j * MF + lrow;
-    if (n >= a.K) continue;
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + n_off + j * MF + lrow;
+      if (n >= a.K) continue;
+      const int lo = (M::row(0, lane) * a.K + n) * 4;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-      for (int e = 0; e < ACC; ++e) {
-        const int m = m0 + m_off + i * MF + M::row(e, lane);
-        if (m < a.npix) o[(int64_t)m * a.K + n] = acc[i][j][e];
-      }
+        for (int e = 0; e < ACC; ++e) {
+          // through a scalar: a bit cast of a vector element read element 0
+          const float v = acc[i][j][e];
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), ro, lo, (i * MF + M::row(e, 0)) * a.K * 4, 0);
+        }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + n_off + j * MF + lrow;
+      if (n >= a.K) continue;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < ACC; ++e) {
+          const int mr = i * MF + M::row(e, lane);
+          if (mw + mr < a.npix) ob[(int64_t)mr * a.K + n] = acc[i][j][e];
+        }
     }
   }
 }

@@ -268,6 +268,8 @@ static int geom_igemm_bf16(const OpX& x, const ct_schedule& s, Geom* g, std::str
     const int steps = kc / (mf == 32 ? 16 : 32);
     if (steps > 4 || steps * (tm + tn) > 16) REJECT("too many fragments held in registers");
   }
+  // the epilogue's buffer stores address a wave tile of y in 32-bit bytes
+  if (4 * x.ny >= ((int64_t)1 << 31)) REJECT("output too large for 32-bit buffer offsets");
   const int64_t chunks = cdiv(o.c, kc);
   int64_t cps = 0;
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty channel range");
@@ -367,6 +369,7 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const int64_t xs_pad = (int64_t)g->a_loads * 64 * nw * vh;
   if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
     REJECT("tensor too large for 32-bit buffer offsets");
+  if (4 * x.ny >= ((int64_t)1 << 31)) REJECT("output too large for 32-bit buffer offsets");
   const int64_t chunks = cdiv(x.cg, cpc);
   int64_t cps = 0;
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty reduction range");

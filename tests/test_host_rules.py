@@ -157,6 +157,14 @@ def test_validator_rejects_documented_cases():
     assert L.ct_validate(op, L.make_schedule(1, [3, 8, 8, 1, 1, 0, 8, 1, 1])) == L.S_INVALID
     # split that leaves an empty channel range (64 channels, ct 32 -> 2 chunks, split 4)
     assert L.ct_validate(op, L.make_schedule(1, [4, 8, 16, 2, 1, 0, 32, 4, 1])) == L.S_INVALID
+    # the MFMA families store through 32-bit buffer offsets: an output of 2^31
+    # bytes or more is refused (here 2^29 + 2^21 fp32 elements, inputs small)
+    big_y = W.Op("big_y", 1, 8, 363, 363, 4096, 1, 1, dtype=W.DT_BF16, layout=W.LAYOUT_NHWC)
+    assert L.ct_validate(big_y, L.make_schedule(3, [16, 1, 1, 1, 1, 32, 0, 1, 0])) == L.S_INVALID
+    assert "output too large" in L.ct_last_error()
+    big_y32 = W.Op("big_y32", 1, 16, 363, 363, 4096, 1, 1)
+    assert L.ct_validate(big_y32, L.make_schedule(4, [16, 1, 1, 1, 4, 1, 32, 16, 1, 1])) == L.S_INVALID
+    assert "output too large" in L.ct_last_error()
     # malformed op
     with pytest.raises(L.CtError):
         L.ct_validate(W.Op("bad", 1, 3, 4, 4, 5, 3, 3, groups=2), bad_threads)
