@@ -288,12 +288,15 @@ def search_study(layers: Sequence[T.LayerData], cands: Dict[int, List[L.ct_sched
                "guided_to_within": first_within(np.where(g_st == L.S_OK, g_lat, np.inf), target),
                "early_stop_measured": e_res["n_measured"], "early_stopped": bool(e_res["stopped_early"]),
                "guided_propose_s": g_res["propose_s"], "guided_measure_s": g_res["measure_s"],
+               "guided_frac_of_scaled_peak": ld.op.flops() / (float(lat[1]) * 1e-6) / 1e12 /
+                                             (T.PEAK_FP32_TFLOPS * fraction),
                "guided_families": {str(f): int(sum(1 for s in g_meas if s.family == f)) for f in (1, 2, 3, 4)},
                "random_families": {str(f): int(sum(1 for s in c if s.family == f)) for f in (1, 2, 3, 4)}}
         out["layers"].append(row)
-        print("search %-7s winners (us) random %.2f guided %.2f early-stop %.2f (%d measured%s); to within %d%%: "
-              "random %d, guided %d; propose %.2fs measure %.2fs" % (
-                  row["layer"], lat[0], lat[1], lat[2], row["early_stop_measured"],
+        print("search %-7s winners (us) random %.2f guided %.2f (%.1f%% of the scaled peak) early-stop %.2f "
+              "(%d measured%s); to within %d%%: random %d, guided %d; propose %.2fs measure %.2fs" % (
+                  row["layer"], lat[0], lat[1], 100 * row["guided_frac_of_scaled_peak"], lat[2],
+                  row["early_stop_measured"],
                   ", stopped" if row["early_stopped"] else "", round(100 * within), row["random_to_within"],
                   row["guided_to_within"], row["guided_propose_s"], row["guided_measure_s"]), flush=True)
     rows = out["layers"]
@@ -316,19 +319,23 @@ def main(argv=None) -> int:
     ap.add_argument("study", choices=("tsi", "isolation", "search"))
     ap.add_argument("--layers", type=int, default=12, help="first N ResNet-18 layers")
     ap.add_argument("--candidates", type=int, default=128)
+    ap.add_argument("--fraction", type=float, default=0.25, help="CU share of the search study")
+    ap.add_argument("--only", default=None, help="comma-separated layer names (default: the first N)")
     ap.add_argument("--out", default=None)
     a = ap.parse_args(argv)
     L.ct_init(0)
     cfg = W.config(2)
     cfg.n_candidates = a.candidates
     layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops[:a.layers])]
+    if a.only:
+        layers = [ld for ld in layers if ld.op.name in a.only.split(",")]
     cands = T.sample_all(layers, cfg)
     if a.study == "tsi":
         rep = tsi_scaling(layers, cands, cfg)
         print("tsi total seconds by k:", json.dumps(rep["total_s"]), "speedup:", json.dumps(rep["speedup"]),
               "winner flips:", rep["winner_flips"], "max gap %.3f" % rep["max_flip_gap"], flush=True)
     elif a.study == "search":
-        rep = search_study(layers, cands, cfg)
+        rep = search_study(layers, cands, cfg, fraction=a.fraction)
         print("search summary:", json.dumps({k: v for k, v in rep.items() if k != "layers"}), flush=True)
     else:
         rep = isolation_study(layers, cands, cfg)
