@@ -135,18 +135,45 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
     const bool ok = e < wt && k0 + kk < K && c < nc;
     return ok ? (((k0 + kk) * C + cc + c) * RS + rs) * 4 : kOob;
   };
-  // Chunks small enough for NS staging elements per thread go through
-  // registers: the next chunk's loads are in flight during this chunk's
-  // MACs, so a block pays one memory round trip per chunk only once.
+  // Chunks of at most NS staging elements per thread (halo and filter
+  // each) go through registers: the next chunk's loads are in flight during
+  // this chunk's MACs, so a block pays one memory round trip per chunk only
+  // once. An element's offset depends on the chunk only through its first
+  // channel cc, which moves the buffer's base instead: the offsets are
+  // computed once, and a chunk's loads take no address arithmetic.
+  // Channels of a last, partial chunk past nc stage values that the MACs
+  // never read.
+  const int nsx = (xt + a.threads - 1) / a.threads, nsw = (wt + a.threads - 1) / a.threads;
   auto prefetched = [&](auto ns) {
     constexpr int NS = decltype(ns)::value;
+    int xo[NS], wo[NS];
+#pragma unroll
+    for (int u = 0; u < NS; ++u) {
+      xo[u] = kOob;
+      wo[u] = kOob;
+      const int e = t + u * a.threads;
+      if (u < nsx) {
+        const int c = qdiv(e, a.inv_plane);
+        const int rem = e - c * plane;
+        const int hh = qdiv(rem, a.inv_iwt), ww = rem - hh * a.iw_t;
+        const int gh = ih_org + hh, gw = iw_org + ww;
+        if (e < xt && (unsigned)gh < (unsigned)H && (unsigned)gw < (unsigned)W) xo[u] = (c * HW + gh * W + gw) * 4;
+      }
+      if (u < nsw) {
+        const int kk = qdiv(e, a.inv_crs);
+        const int rem = e - kk * crs;
+        const int c = qdiv(rem, a.inv_rs), rs = rem - c * RS;
+        if (e < wt && k0 + kk < K) wo[u] = ((k0 + kk) * C * RS + c * RS + rs) * 4;
+      }
+    }
     float px[NS], pw[NS];
     auto fetch = [&](const int cc) {
-      const int nc = min(a.ct, c_end - cc);
+      const __amdgpu_buffer_rsrc_t rxc = make_rsrc(xn + (int64_t)cc * HW, (int64_t)(C - cc) * HW * 4);
+      const __amdgpu_buffer_rsrc_t rwc = make_rsrc(w + (int64_t)cc * RS, ((int64_t)K * C - cc) * RS * 4);
 #pragma unroll
       for (int u = 0; u < NS; ++u) {
-        px[u] = bload1(rx, x_off(t + u * a.threads, cc, nc));
-        pw[u] = bload1(rwt, w_off(t + u * a.threads, cc, nc));
+        if (u < nsx) px[u] = bload1(rxc, xo[u]);
+        if (u < nsw) pw[u] = bload1(rwc, wo[u]);
       }
     };
     float* xs = smem;
@@ -156,8 +183,8 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
 #pragma unroll
       for (int u = 0; u < NS; ++u) {
         const int e = t + u * a.threads;
-        if (e < xt) xs[e] = px[u];
-        if (e < wt) wsm[e] = pw[u];
+        if (u < nsx && e < xt) xs[e] = px[u];
+        if (u < nsw && e < wt) wsm[e] = pw[u];
       }
       __syncthreads();
       if (cc + a.ct < c_end) fetch(cc + a.ct);
@@ -165,13 +192,29 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
       __syncthreads();  // the next chunk's stores overwrite the tiles
     }
   };
-  const int n_stage = (max(xt, wt) + a.threads - 1) / a.threads;
   bool done = false;
-  if constexpr (LDS && MK * MW < 8) {  // registers to spare beside the accumulators
-    done = true;
-    if (n_stage <= 1) prefetched(std::integral_constant<int, 1>{});
-    else if (n_stage <= 2) prefetched(std::integral_constant<int, 2>{});
-    else done = false;
+  if constexpr (LDS) {
+    // the deepest prefetch that leaves the MACs their registers: 16 elements
+    // per thread where the launch bound gives 256 VGPRs, else 8, or beside
+    // two unrolled channels 4 (4 accumulators) or none (8)
+    constexpr int kMaxNs = direct_max_threads(MK * MW) <= 512 ? 16
+                           : UNR == 2 && MK * MW >= 8 ? 0
+                           : UNR == 2 && MK * MW >= 4 ? 4 : 8;
+    const int n_stage = max(nsx, nsw);
+    done = kMaxNs > 0 && n_stage <= kMaxNs;
+    if constexpr (kMaxNs > 0) {
+      if (n_stage <= 2) {
+        prefetched(std::integral_constant<int, 2>{});
+      } else if (n_stage <= 4) {
+        prefetched(std::integral_constant<int, 4>{});
+      } else if constexpr (kMaxNs >= 8) {
+        if (n_stage <= 8) {
+          prefetched(std::integral_constant<int, 8>{});
+        } else if constexpr (kMaxNs >= 16) {
+          if (n_stage <= 16) prefetched(std::integral_constant<int, 16>{});
+        }
+      }
+    }
   }
 
   for (int cc = c_begin; cc < c_end && !done; cc += a.ct) {
@@ -219,6 +262,44 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
         const float* wrow[MK];
 #pragma unroll
         for (int i = 0; i < MK; ++i) wrow[i] = w + min(kb + i, K - 1) * C * RS;
+        if constexpr (RC != 0) {
+          // fixed filter: this thread's input offset at every tap and column
+          // is the same in every channel plane (kOob in the padding), so it
+          // is computed once and a channel moves the buffer's base
+          int xo[RC][RC][MW];
+#pragma unroll
+          for (int r = 0; r < RC; ++r) {
+            const int gh = oh * sh - ph + r;
+            const bool hok = (unsigned)gh < (unsigned)H && oh < a.OH;
+#pragma unroll
+            for (int s = 0; s < RC; ++s)
+#pragma unroll
+              for (int j = 0; j < MW; ++j) {
+                const int gw = (ow0 + lc + j * a.cols) * sw - pw + s;
+                xo[r][s][j] = hok && (unsigned)gw < (unsigned)W ? (gh * W + gw) * 4 : kOob;
+              }
+          }
+#pragma unroll UNR
+          for (int c = 0; c < nc; ++c) {
+            const __amdgpu_buffer_rsrc_t rxc = make_rsrc(xn + (int64_t)(cc + c) * HW, (int64_t)HW * 4);
+            const int co = (cc + c) * RS;
+#pragma unroll
+            for (int r = 0; r < RC; ++r)
+#pragma unroll
+              for (int s = 0; s < RC; ++s) {
+                float xv[MW], wv[MK];
+#pragma unroll
+                for (int j = 0; j < MW; ++j) xv[j] = bload1(rxc, xo[r][s][j]);
+#pragma unroll
+                for (int i = 0; i < MK; ++i) wv[i] = wrow[i][co + r * RC + s];
+#pragma unroll
+                for (int i = 0; i < MK; ++i)
+#pragma unroll
+                  for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+              }
+          }
+          return;
+        }
 #pragma unroll UNR
         for (int c = 0; c < nc; ++c) {
           const int xo = (cc + c) * HW;
