@@ -38,6 +38,8 @@ from collections import defaultdict
 CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 
 # kernel name prefix -> the source files that define it
+PEAK_FP32_TFLOPS = 157.3  # MI355X dense fp32 (vector and MFMA), 256 CUs at 2.4 GHz
+
 _KERNEL_SOURCES = {
     "direct_f32_kernel": ["k_direct*"],
     "depthwise_f32_kernel": ["k_depthwise*"],
@@ -244,15 +246,20 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
             lines.append("No dispatch of that kernel with that shape is in the trace.")
     if replay:
         lines += ["", "## Replay (kernel alone)", "",
-                  "`%s`, %d launches at %.0f%% of the CUs: %.3f us by HIP events, %.2f TFLOP/s." % (
+                  "`%s`, %d launches at %g%% of the CUs: %.3f us by HIP events, %.2f TFLOP/s." % (
                       replay["kernel"], replay["launches"], 100 * replay["fraction"], replay["latency_us"],
                       replay["tflops"])]
         sh = replay["schedule"]
         rdurs = tr.durations(replay["kernel"], sh.get("threads"), sh.get("blocks", 0) * sh.get("threads", 0),
                              sh.get("lds_bytes"))
         if rdurs:
-            lines.append("Trace of the replay: %d launches, avg %.3f us, median %.3f us." % (
-                len(rdurs), statistics.mean(rdurs) / 1e3, statistics.median(rdurs) / 1e3))
+            tavg = statistics.mean(rdurs) / 1e3
+            ttf = replay["tflops"] * replay["latency_us"] / tavg  # the launch's FLOP over the trace average
+            lines.append("Trace of the replay: %d launches, avg %.3f us, median %.3f us; from the average %.2f "
+                         "TFLOP/s = %.1f%% of the fp32 peak scaled to the share (%.1f x %g)." % (
+                             len(rdurs), tavg, statistics.median(rdurs) / 1e3, ttf,
+                             100 * ttf / (PEAK_FP32_TFLOPS * replay["fraction"]), PEAK_FP32_TFLOPS,
+                             replay["fraction"]))
             if sh.get("kernels", 1) > 1:
                 red = tr.durations("split_reduce_kernel", None, None)
                 if red:
