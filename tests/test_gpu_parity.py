@@ -145,28 +145,42 @@ def test_every_family_covered_on_config1_shape():
         check_close(op, yd.cpu().numpy(), ref, a, "config1 " + sched_str(s), split=4)
 
 
+def _fixed_filter(op):
+    """The 1x1 / 3x3 specialisations (stride 1 or 2, no dilation, 'same' padding)."""
+    sq = op.r == op.s and op.stride_h == op.stride_w and op.stride_h in (1, 2) and op.dil_h == op.dil_w == 1
+    return sq and ((op.r == 1 and op.pad_h == op.pad_w == 0) or (op.r == 3 and op.pad_h == op.pad_w == 1))
+
+
 def _direct_class(op, s):
-    """Which staging path a direct schedule takes (mirrors the kernel's choice)."""
-    toh, tow, tk, mk, mw, lds, ct = (s.knob[i] for i in range(7))
+    """Which operand path a direct schedule takes (mirrors the kernel's choice)."""
+    toh, tow, tk, mk, mw, lds, ct, split, unr = (s.knob[i] for i in range(9))
     cols = tow // mw
     threads = (tk // mk) * toh * cols
     if not lds:
-        return "regs-uniform-w" if (toh * cols) % 64 == 0 else "regs"
+        kind = "regs-fixed" if _fixed_filter(op) else "regs"
+        return kind + ("-uniform-w" if (toh * cols) % 64 == 0 else "")
     ih = (toh - 1) * op.stride_h + (op.r - 1) * op.dil_h + 1
     iw = (tow - 1) * op.stride_w + (op.s - 1) * op.dil_w + 1
     xt, wt = ct * ih * iw, tk * ct * op.r * op.s
-    n_stage = (max(xt, wt) + threads - 1) // threads
-    if mk * mw < 8 and n_stage <= 2:
-        return "prefetch-%d" % n_stage
+    n_stage = max(-(-xt // threads), -(-wt // threads))
+    tile = mk * mw
+    # deepest register prefetch the instance allows (launch bound 512 threads
+    # from 16 accumulators up, else 1024)
+    cap = 16 if tile >= 16 else (0 if unr == 2 and tile >= 8 else (4 if unr == 2 and tile >= 4 else 8))
+    if cap and n_stage <= cap:
+        return "prefetch-%d" % next(d for d in (2, 4, 8, 16) if n_stage <= d)
     return "batch16" if n_stage >= 16 else "batch4"
 
 
-@pytest.mark.parametrize("op", [W.conv("deep3x3", 1, 48, 9, 72, 3, 1), F32_OPS[1], F32_OPS[5]],
+@pytest.mark.parametrize("op", [W.conv("deep3x3", 1, 48, 9, 72, 3, 1), F32_OPS[1], F32_OPS[4], F32_OPS[5]],
                          ids=lambda o: o.name)
 def test_direct_staging_paths_match_oracle(op):
-    # every way the direct family reads its operands: registers with vector or
-    # scalar filter loads, LDS chunks through registers (one or two elements
-    # per thread), and LDS staging in batches of four or sixteen loads
+    # every way the direct family reads its operands: registers (per-tap
+    # input offsets kept resident for a fixed 1x1 or 3x3 filter) with vector
+    # or scalar filter loads, LDS chunks prefetched through registers at each
+    # depth (2, 4, 8, 16 elements per thread; a last chunk shorter than CT
+    # where C is not a multiple of it, split channel ranges), and LDS staging
+    # in batches of four or sixteen loads
     x, w = make_inputs(op, "uniform", seed=31)
     ref, a = reference(op, x, w)
     xd, wd, yd = to_device(op, x, w)
@@ -176,8 +190,15 @@ def test_direct_staging_paths_match_oracle(op):
             by.setdefault(_direct_class(op, s), []).append(s)
     rng = random.Random(5)
     seen = set()
+    ragged = 0
     for cls in sorted(by):
-        for s in rng.sample(by[cls], min(3, len(by[cls]))):
+        pool = by[cls]
+        # prefer schedules whose channel chunks do not divide C, then split ones
+        pick = rng.sample(pool, min(3, len(pool)))
+        odd = [s for s in pool if op.c % s.knob[6] and s not in pick]
+        spl = [s for s in pool if s.knob[7] > 1 and s not in pick]
+        pick += rng.sample(odd, min(2, len(odd))) + rng.sample(spl, min(1, len(spl)))
+        for s in pick:
             tag = "%s %s [%s]" % (op.name, sched_str(s), cls)
             note(tag)
             yd.fill_(float("nan"))
@@ -185,9 +206,12 @@ def test_direct_staging_paths_match_oracle(op):
             split = L.ct_launch_shape(op, s)["kernels"]
             check_close(op, yd.cpu().numpy(), ref, a, tag, split=4 if split > 1 else 1)
             seen.add(cls)
-    print(op.name, "paths:", sorted(seen))
+            ragged += bool(op.c % s.knob[6]) and cls.startswith("prefetch")
+    print(op.name, "paths:", sorted(seen), "ragged prefetched chunks:", ragged)
     if op.name == "deep3x3":
-        assert {"regs", "prefetch-1", "prefetch-2", "batch4", "batch16"} <= seen
+        assert {"regs-fixed", "prefetch-2", "prefetch-4", "prefetch-8", "prefetch-16", "batch4",
+                "batch16"} <= seen
+        assert ragged > 0
 
 
 # Degenerate shapes: a one-pixel image (only the centre tap of a padded 3x3
