@@ -52,12 +52,17 @@ extern "C" {
 #define CT_E_NOINIT   -3   /* ct_init() has not succeeded                        */
 #define CT_E_OOM      -4   /* workspace allocation failed                        */
 #define CT_E_NODEV    -5   /* no usable gfx950 device                            */
+#define CT_E_TIMEOUT  -6   /* a candidate ran past its time limit and its stream */
+                           /* did not drain within the grace period: the call    */
+                           /* gave up waiting (its stream is never reused)        */
+#define CT_E_CLIENT   -7   /* a tuning client thread stopped on an exception     */
+#define CT_E_STOPPED  -8   /* a client was stopped by a test hook (host tests)   */
 
 /* ---- per-candidate status codes (status[] outputs) ---- */
 #define CT_S_OK           0
 #define CT_S_INVALID      1  /* rejected by the validator; never launched, latency +inf */
 #define CT_S_LAUNCH       2  /* the launch itself failed                                */
-#define CT_S_TIMEOUT      3  /* measured latency above the protocol's time limit        */
+#define CT_S_TIMEOUT      3  /* a run took longer than the protocol's time limit        */
 #define CT_S_WRONG_ANSWER 4  /* output differs from the reference beyond tolerance      */
 
 /* ---- kernel families ---- */
@@ -95,8 +100,16 @@ typedef struct ct_schedule {
 /* Timing protocol. Each candidate: `warmup` untimed runs, then `repeats`
  * repeats of (event record; `launches` back-to-back runs; event record).
  * Latency = median over repeats of (elapsed / launches). Candidates are
- * enqueued in groups of `batch` with one stream synchronisation per group.
- * A candidate whose latency exceeds timeout_ms gets CT_S_TIMEOUT. */
+ * enqueued in groups of `batch`; the host then waits for the group's events
+ * in order, polling each against a deadline: the runs enqueued before an
+ * event may take at most timeout_ms each (plus 50 ms of slack for the host's
+ * own scheduling), counted from when the previous event was seen complete.
+ * A candidate whose runs pass that deadline, or whose median latency exceeds
+ * timeout_ms, gets CT_S_TIMEOUT. Kernels already enqueued cannot be recalled:
+ * after a deadline passes the host waits for the stream to drain for
+ * max(2 s, 4 x the remaining runs x timeout_ms), at most 60 s; if it drains
+ * the other candidates keep their measurements, otherwise the call returns
+ * CT_E_TIMEOUT and the stream is abandoned. */
 typedef struct ct_measure_opts {
     int32_t warmup;
     int32_t repeats;     /* 1..64 */
@@ -145,6 +158,9 @@ int ct_cu_mask(double fraction, int slot, uint32_t *mask, int words);
 int ct_grid_info(int family, int32_t *num_knobs, int64_t *grid_size);
 /* Value list of knob `knob` of `family`: writes up to cap values, sets *count. */
 int ct_knob_values(int family, int knob, int32_t *values, int32_t cap, int32_t *count);
+/* Number of schedules of `family` that the validator accepts for op (0 if the
+ * family does not apply to op's layout, dtype or grouping). */
+int ct_grid_size(const ct_op *op, int family, int64_t *n);
 /* Mixed-radix decode/encode: the first knob is the most significant digit. */
 int ct_grid_decode(int family, int64_t index, ct_schedule *out);
 int ct_grid_encode(const ct_schedule *s, int64_t *index);
@@ -212,6 +228,18 @@ int measure_candidates_mask(const ct_op *op, const ct_schedule *s, int n,
                             const ct_verify *v, const void *x, const void *w, void *y,
                             float *lat_us, int32_t *status, float *rep_us);
 
+/* Register the exact output of op for later measurements (the runner's
+ * correctness check): y_ref_host is N*OH*OW*K fp64 values in op's output
+ * layout (host memory, read during the call only). The library rounds them
+ * to fp32 and keeps one device copy per op (ops compare field by field).
+ * From then on every measurement of that op without an explicit ct_verify
+ * reference re-runs each candidate once after its timed runs and sets
+ * CT_S_WRONG_ANSWER when max|y - ref| > tol * max|ref| (tol 1e-4 for fp32 ops,
+ * 2e-2 for bf16 ops). The reference holds only for the x and w it was
+ * computed from: the caller keeps them. y_ref_host = NULL removes the op's
+ * reference. Released by ct_shutdown. */
+int ct_set_reference(const ct_op *op, const double *y_ref_host);
+
 /* ---- selection (stage 4 of the loop; the best configuration is the one
  *      with the lowest measured latency, as the early-stop rule implies) ---- */
 
@@ -240,6 +268,13 @@ typedef struct ct_tune_job {
     int32_t winner_pos;                  /* out: sample position of the winner, -1 if none */
     float   winner_lat_us;               /* out */
     double  t_start_s, t_end_s;          /* out: steady-clock seconds           */
+    int32_t layer_id;                    /* in: the layer's id, written to logs */
+    const uint8_t *skip;                 /* in, optional [n_cands]: candidates  */
+                                         /* with skip[i] != 0 are not measured; */
+                                         /* lat1_us[i] / status1[i] must hold   */
+                                         /* their recorded values (resume)      */
+    int32_t rc;                          /* out: 0, or the CT_E_* code that     */
+                                         /* stopped this job                    */
 } ct_tune_job;
 
 /* One tuning client: a host thread that owns a CU-masked stream and tunes
@@ -252,12 +287,28 @@ typedef struct ct_client {
     int32_t rc;                          /* out: 0 or a CT_E_* code             */
     double t_start_s, t_end_s;           /* out: first job start, last job end  */
     int64_t n_measured;                  /* out: candidates screened            */
+    const char *log_path;                /* in, optional: append-only JSON-lines */
+                                         /* log of this client (below); NULL =  */
+                                         /* none                                */
+    double cands_per_s;                  /* out: n_measured / (t_end - t_start) */
 } ct_client;
 
 /* Run n_clients clients concurrently, one host thread each, and wait for all.
  * Clients with overlapping masks are allowed but then share CUs. With the
  * environment variable CT_PROGRESS set, each client writes one line to stderr
- * per finished job. */
+ * per finished job.
+ *
+ * Logs (section 3.1.1: each tuning client keeps its own log and the logs are
+ * merged per model). A client with log_path appends one JSON object per line
+ * and flushes after each group of measured candidates:
+ *   {"kind":"cand","layer":L,"pos":P,"family":F,"knobs":[...],"lat_us":X,"status":S}
+ * for every screened candidate (X is null when not finite), and after a job
+ * {"kind":"job","layer":L,"n_cands":N,"winner_pos":P,"winner_lat_us":X,
+ *  "top_pos":[...],"lat2_us":[...],"rc":R}.
+ * Candidate lists are a pure function of (seed, configuration, layer), so a
+ * run is resumed by passing the recorded candidates through the job's skip
+ * array. A client that fails (rc < 0) stops; the others keep taking jobs. An
+ * exception inside a client thread is caught and reported as CT_E_CLIENT. */
 int ct_tune_clients(ct_client *clients, int n_clients, const ct_measure_opts *stage1,
                     const ct_measure_opts *stage2, float eps);
 
@@ -271,6 +322,26 @@ int ct_tune_clients(ct_client *clients, int n_clients, const ct_measure_opts *st
 int ct_tune_shared(ct_client *clients, int n_clients, ct_tune_job *jobs, int n_jobs,
                    const ct_measure_opts *stage1, const ct_measure_opts *stage2, float eps,
                    int32_t *job_client);
+
+/* Aggregate throughput of clients that have run: the sum of n_measured over
+ * (latest t_end_s - earliest t_start_s), the conservative "time taken to
+ * finish all of them" reading of the paper's throughput. Host only. */
+int ct_throughput(const ct_client *clients, int n_clients, double *cands_per_s);
+
+/* One client, one layer, k tuning server instances (section 3.1.1, Fig. 7a):
+ * the job's candidate list is split into k contiguous parts, part j =
+ * sample positions [n j / k, n (j + 1) / k), screened concurrently (one host
+ * thread per part) on masks[j] (words words each) with output buffer
+ * y_slots[j]; the k results are merged in place in lat1_us / status1, the
+ * job's top_t are re-measured with stage2 on masks[0] (into y_slots[0]) and
+ * the winner selected as in ct_tune_clients. y_slots holds k device buffers
+ * the size of y (distinct, so that concurrent parts do not write the same
+ * output); y_slots[0] may be job->y. screen_s (optional out) = wall seconds
+ * of the concurrent screening. The job's verify reference (or the op's
+ * registered one) checks every part. */
+int ct_tune_split(ct_tune_job *job, const uint32_t *masks, int k, int words, void *const *y_slots,
+                  const ct_measure_opts *stage1, const ct_measure_opts *stage2, float eps,
+                  double *screen_s);
 
 /* ---- cross-evaluation (section 2.2.1, Tables 1-2: tuned at f, run at g) ---- */
 
@@ -357,6 +428,39 @@ int ct_probe_empty(const uint32_t *cu_mask, int words, int blocks, const ct_meas
  * device-to-device copy kernel on the mask, in GB/s. Buffers are the caller's. */
 int ct_probe_copy(const uint32_t *cu_mask, int words, const void *src, void *dst, int64_t bytes,
                   const ct_measure_opts *o, float *gbps);
+
+/* Number of CU-masked streams the library holds. A stream is reused by later
+ * calls with the same mask once the call holding it returns, so the count is
+ * bounded by the most calls that ran at once on one mask (diagnostic). */
+int ct_stream_count(void);
+
+/* ---- host-logic test hooks (no device work) ----
+ * These drive the library's own host code -- client threads, the shared job
+ * queue, logs, resume, top-t selection and the timeout watchdog -- with a
+ * stand-in for the device, so that failure handling is tested on a machine
+ * without a GPU. They never compute a convolution. */
+
+typedef struct ct_test_hooks {
+    int32_t delay_us;           /* host sleep per stand-in measurement              */
+    int32_t throw_client;       /* client that raises an exception (-1: none) ...   */
+    int32_t throw_after_jobs;   /* ... when it starts its job number k (0-based)    */
+    int64_t stop_after_records; /* every client stops (CT_E_STOPPED) once this many */
+                                /* candidate records are logged in total (-1: never) */
+} ct_test_hooks;
+
+/* ct_tune_shared with the stand-in measurement: candidate i of a job gets
+ * status CT_S_OK and latency 1 + ((layer_id * 7919 + i) * 2654435761 mod 1000)
+ * / 100 microseconds after hooks->delay_us of host sleep; the re-measure
+ * repeats the same latency. Needs no ct_init. */
+int ct_test_run_clients(ct_client *clients, int n_clients, ct_tune_job *jobs, int n_jobs,
+                        const ct_test_hooks *hooks, int32_t *job_client);
+
+/* The timeout watchdog on a simulated stream: event k completes at
+ * done_at_s[k] seconds (< 0: never); runs[k] runs precede it; the host polls
+ * every millisecond of simulated time. Outputs the first event whose
+ * deadline passed (-1: none) and whether the stream drained afterwards. */
+int ct_test_watchdog(int n_events, const int32_t *runs, const double *done_at_s, double run_limit_s,
+                     double slack_s, double drain_cap_s, int32_t *expired_event, int32_t *drained);
 
 #ifdef __cplusplus
 }

@@ -8,6 +8,7 @@ Loading fails loudly when the library is missing: there is no fallback.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
 import threading
@@ -18,6 +19,7 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libconvtune.so")
 
 CT_OK, CT_E_ARG, CT_E_HIP, CT_E_NOINIT, CT_E_OOM, CT_E_NODEV = 0, -1, -2, -3, -4, -5
+CT_E_TIMEOUT, CT_E_CLIENT, CT_E_STOPPED = -6, -7, -8
 S_OK, S_INVALID, S_LAUNCH, S_TIMEOUT, S_WRONG_ANSWER = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "ok", 1: "invalid", 2: "launch_error", 3: "timeout", 4: "wrong_answer"}
 MASK_WORDS = 8
@@ -57,13 +59,19 @@ class ct_tune_job(ctypes.Structure):
                 ("cands", P(ct_schedule)), ("n_cands", c_i32), ("verify", ct_verify),
                 ("lat1_us", P(c_f32)), ("status1", P(c_i32)), ("top_t", c_i32),
                 ("top_pos", P(c_i32)), ("lat2_us", P(c_f32)), ("n_top", c_i32), ("winner_pos", c_i32),
-                ("winner_lat_us", c_f32), ("t_start_s", c_f64), ("t_end_s", c_f64)]
+                ("winner_lat_us", c_f32), ("t_start_s", c_f64), ("t_end_s", c_f64), ("layer_id", c_i32),
+                ("skip", P(ctypes.c_uint8)), ("rc", c_i32)]
 
 
 class ct_client(ctypes.Structure):
     _fields_ = [("cu_mask", c_u32 * MASK_WORDS), ("host_core", c_i32), ("jobs", P(ct_tune_job)),
                 ("n_jobs", c_i32), ("rc", c_i32), ("t_start_s", c_f64), ("t_end_s", c_f64),
-                ("n_measured", c_i64)]
+                ("n_measured", c_i64), ("log_path", ctypes.c_char_p), ("cands_per_s", c_f64)]
+
+
+class ct_test_hooks(ctypes.Structure):
+    _fields_ = [("delay_us", c_i32), ("throw_client", c_i32), ("throw_after_jobs", c_i32),
+                ("stop_after_records", c_i64)]
 
 
 class ct_search_opts(ctypes.Structure):
@@ -84,6 +92,14 @@ _SIGS = {
     "ct_build_cu_mask": (c_i32, [c_i32, c_f64, c_i32, P(c_u32), c_i32]),
     "ct_cu_mask": (c_i32, [c_f64, c_i32, P(c_u32), c_i32]),
     "ct_grid_info": (c_i32, [c_i32, P(c_i32), P(c_i64)]),
+    "ct_grid_size": (c_i32, [P(ct_op), c_i32, P(c_i64)]),
+    "ct_set_reference": (c_i32, [P(ct_op), P(c_f64)]),
+    "ct_throughput": (c_i32, [P(ct_client), c_i32, P(c_f64)]),
+    "ct_tune_split": (c_i32, [P(ct_tune_job), P(c_u32), c_i32, c_i32, P(ctypes.c_void_p), P(ct_measure_opts),
+                              P(ct_measure_opts), c_f32, P(c_f64)]),
+    "ct_stream_count": (c_i32, []),
+    "ct_test_run_clients": (c_i32, [P(ct_client), c_i32, P(ct_tune_job), c_i32, P(ct_test_hooks), P(c_i32)]),
+    "ct_test_watchdog": (c_i32, [c_i32, P(c_i32), P(c_f64), c_f64, c_f64, c_f64, P(c_i32), P(c_i32)]),
     "ct_knob_values": (c_i32, [c_i32, c_i32, P(c_i32), c_i32, P(c_i32)]),
     "ct_grid_decode": (c_i32, [c_i32, c_i64, P(ct_schedule)]),
     "ct_grid_encode": (c_i32, [P(ct_schedule), P(c_i64)]),
@@ -135,6 +151,9 @@ def lib():
                 f.restype = res
                 f.argtypes = args
             _lib = h
+            # streams, events and workspaces go back before the HIP runtime's
+            # own teardown at process exit (ct_shutdown is safe to call twice)
+            atexit.register(h.ct_shutdown)
     return _lib
 
 
@@ -212,6 +231,10 @@ def ct_shutdown() -> None:
     lib().ct_shutdown()
 
 
+def ct_stream_count() -> int:
+    return _check(lib().ct_stream_count())
+
+
 def ct_last_error() -> str:
     return lib().ct_last_error().decode(errors="replace")
 
@@ -232,6 +255,25 @@ def ct_grid_info(family: int):
     nk, gs = c_i32(), c_i64()
     _check(lib().ct_grid_info(family, ctypes.byref(nk), ctypes.byref(gs)))
     return nk.value, gs.value
+
+
+def ct_grid_size(op, family: int) -> int:
+    """Number of schedules of `family` the validator accepts for op."""
+    o = make_op(op)
+    n = c_i64()
+    _check(lib().ct_grid_size(ctypes.byref(o), family, ctypes.byref(n)))
+    return n.value
+
+
+def ct_set_reference(op, y_ref_host: Optional[np.ndarray]) -> None:
+    """Register op's exact output (fp64, op's output layout) for later
+    measurements; None removes it."""
+    o = make_op(op)
+    if y_ref_host is None:
+        _check(lib().ct_set_reference(ctypes.byref(o), None))
+        return
+    ref = np.ascontiguousarray(y_ref_host, dtype=np.float64)
+    _check(lib().ct_set_reference(ctypes.byref(o), _arr(ref, c_f64)))
 
 
 def ct_knob_values(family: int, knob: int) -> List[int]:
@@ -357,6 +399,46 @@ def ct_tune_shared(clients: ctypes.Array, jobs: ctypes.Array, opts1: ct_measure_
     _check(lib().ct_tune_shared(clients, len(clients), jobs, len(jobs), ctypes.byref(opts1), ctypes.byref(opts2),
                                 eps, _arr(owner, c_i32)))
     return owner[:len(jobs)]
+
+
+def ct_throughput(clients: ctypes.Array) -> float:
+    """Aggregate candidates/s of clients that have run (sum over the makespan)."""
+    v = c_f64()
+    _check(lib().ct_throughput(clients, len(clients), ctypes.byref(v)))
+    return v.value
+
+
+def ct_tune_split(job: ct_tune_job, masks: Sequence, y_slots: Sequence, opts1: ct_measure_opts,
+                  opts2: ct_measure_opts, eps: float) -> float:
+    """Screen one job's candidates on len(masks) CU slots at once, merge, then
+    re-measure and select on slot 0; returns the screening seconds."""
+    k = len(masks)
+    mk = np.ascontiguousarray(np.array(masks, dtype=np.uint32).reshape(k, MASK_WORDS))
+    ys = (ctypes.c_void_p * k)(*[_ptr(y) for y in y_slots])
+    sec = c_f64()
+    _check(lib().ct_tune_split(ctypes.byref(job), _arr(mk, c_u32), k, MASK_WORDS, ys, ctypes.byref(opts1),
+                               ctypes.byref(opts2), eps, ctypes.byref(sec)))
+    return sec.value
+
+
+def ct_test_run_clients(clients: ctypes.Array, jobs: ctypes.Array, hooks: ct_test_hooks) -> np.ndarray:
+    """The client machinery with the library's stand-in measurement (host only);
+    returns the client index per job. Raises CtError with the call's code."""
+    owner = np.full(max(len(jobs), 1), -1, dtype=np.int32)
+    _check(lib().ct_test_run_clients(clients, len(clients), jobs, len(jobs), ctypes.byref(hooks),
+                                     _arr(owner, c_i32)))
+    return owner[:len(jobs)]
+
+
+def ct_test_watchdog(runs: Sequence[int], done_at_s: Sequence[float], run_limit_s: float, slack_s: float,
+                     drain_cap_s: float):
+    """The timeout watchdog on a simulated stream: (expired event or -1, drained)."""
+    r = np.ascontiguousarray(runs, dtype=np.int32)
+    d = np.ascontiguousarray(done_at_s, dtype=np.float64)
+    ex, dr = c_i32(), c_i32()
+    _check(lib().ct_test_watchdog(len(r), _arr(r, c_i32), _arr(d, c_f64), run_limit_s, slack_s, drain_cap_s,
+                                  ctypes.byref(ex), ctypes.byref(dr)))
+    return ex.value, bool(dr.value)
 
 
 def ct_cross_eval(op, scheds: Sequence, masks: Sequence, opts: ct_measure_opts, x, w, y) -> np.ndarray:

@@ -4,8 +4,11 @@
 // schedule that validates is launched exactly as it was checked.
 #pragma once
 
+#include <atomic>
 #include <cstdint>
+#include <functional>
 #include <string>
+#include <vector>
 
 #include "convtune.h"
 
@@ -102,6 +105,92 @@ int launch_split_reduce(const float* ws, float* y, int64_t n, int split, void* s
 
 // ---- host rules shared by the C ABI ----
 void set_error(const std::string& msg);
+const std::string& last_error();
 uint64_t splitmix64_next(uint64_t* state);
+double now_s();  // steady clock, seconds
+
+// ---- tuning clients (clients.cpp, host only) ----
+// Receives a job's per-candidate results as they become final, and the job's
+// end. Returns false when the client has to stop (a test hook).
+class RecordSink {
+ public:
+  virtual ~RecordSink() = default;
+  virtual bool candidates(const ct_tune_job& j, int i0, int i1) = 0;
+  virtual void job_done(const ct_tune_job& j) = 0;
+};
+
+// Runs one job for client `ci`; returns CT_OK or a CT_E_* code.
+using JobFn = std::function<int(int ci, ct_tune_job* j, RecordSink* sink)>;
+// Called once per client thread after its last job (releases per-client state).
+using ClientEndFn = std::function<void(int ci)>;
+
+// The jobs a client runs: its own list in order, or (next != nullptr) the
+// next unclaimed job of a queue shared by all clients.
+struct JobSource {
+  ct_tune_job* jobs;
+  int n;
+  std::atomic<int>* next;
+  int32_t* owner;  // shared queue: owner[i] = index of the client that ran job i
+};
+
+// One host thread per client; returns CT_OK or the first failing client's code.
+int run_clients(ct_client* clients, int n_clients, const std::vector<JobSource>& src, const JobFn& fn,
+                const ClientEndFn& on_end, int64_t stop_after_records);
+
+// Stage 2 and selection of a job whose stage-1 results are in place:
+// remeasure(positions, n, lat2) fills lat2 (+inf where not OK).
+int select_job(ct_tune_job* j, float eps,
+               const std::function<int(const int32_t* pos, int n, float* lat2)>& remeasure);
+
+// ---- timeout watchdog ----
+// Waits for n events of one in-order stream. runs[k] kernel runs were
+// enqueued between event k-1 (or the start) and event k; each may take at most
+// run_limit_s, so event k is due run_limit_s * runs[k] + slack_s after event
+// k-1 was seen complete. done(k) reports completion (and may fail with a
+// negative code). On the first missed deadline the watchdog records the event
+// and waits up to drain_cap_s for the last event.
+struct WatchResult {
+  int rc = 0;            // 0, or a negative code from done()
+  int expired = -1;      // first event past its deadline, -1 if none
+  bool drained = true;   // the last event completed
+};
+template <class DoneFn, class ClockFn, class NapFn>
+WatchResult watch_events(int n, const int32_t* runs, double run_limit_s, double slack_s,
+                         double drain_cap_s, DoneFn done, ClockFn now, NapFn nap) {
+  WatchResult r;
+  if (n <= 0) return r;
+  double t_prev = now();
+  int k = 0;
+  while (k < n) {
+    // in an in-order stream the last event completing means all did
+    int d = done(n - 1);
+    if (d < 0) { r.rc = d; return r; }
+    if (d) return r;
+    d = done(k);
+    if (d < 0) { r.rc = d; return r; }
+    if (d) {
+      t_prev = now();
+      ++k;
+      continue;
+    }
+    if (now() > t_prev + run_limit_s * (double)runs[k] + slack_s) {
+      r.expired = k;
+      break;
+    }
+    nap();
+  }
+  if (r.expired < 0) return r;
+  const double t0 = now();
+  for (;;) {
+    const int d = done(n - 1);
+    if (d < 0) { r.rc = d; return r; }
+    if (d) return r;
+    if (now() > t0 + drain_cap_s) {
+      r.drained = false;
+      return r;
+    }
+    nap();
+  }
+}
 
 }  // namespace ct

@@ -1,11 +1,11 @@
-// Host runtime of libconvtune: device set-up, per-thread CU-masked streams,
-// the timing protocol (profile stage of the tuning loop), tuning clients on
-// disjoint CU masks, cross-evaluation and the probes.
+// Host runtime of libconvtune: device set-up, the pool of CU-masked streams,
+// the timing protocol (profile stage of the tuning loop) with its timeout
+// watchdog, registered references, tuning clients on disjoint CU masks (the
+// thread machinery is in clients.cpp), one client over several CU slots,
+// cross-evaluation and the probes.
 #include <hip/hip_runtime.h>
 #include <cstdio>
 #include <cstdlib>
-#include <pthread.h>
-#include <sched.h>
 
 #include <algorithm>
 #include <array>
@@ -29,10 +29,6 @@ int launch_cu_probe(int* out, int nblocks, hipStream_t st);
 int launch_empty(int nblocks, hipStream_t st);
 int launch_copy(const void* src, void* dst, int64_t bytes, int nblocks, hipStream_t st);
 
-// ------------------------------------------------------------------ errors
-static thread_local std::string t_err;
-void set_error(const std::string& msg) { t_err = msg; }
-
 static int hip_fail(const char* what, hipError_t e) {
   set_error(std::string(what) + ": " + hipGetErrorString(e));
   return CT_E_HIP;
@@ -44,15 +40,18 @@ static int hip_fail(const char* what, hipError_t e) {
   } while (0)
 
 // ------------------------------------------------------------------ device
-static std::mutex g_mu;
+static std::mutex g_mu;  // guards the device state, the stream pool and the references
 static int g_device = -1;
 static int g_num_cus = 0;
-static std::atomic<int> g_generation{0};
 
 using MaskKey = std::array<uint32_t, CT_MASK_WORDS>;
 
-// One CU-masked stream with everything a measurement needs on it.
+// One CU-masked stream with everything a measurement needs on it. A context
+// is held by one call at a time (in_use) and returned to the pool after it.
 struct StreamCtx {
+  MaskKey key{};
+  bool in_use = false;
+  bool abandoned = false;  // a wait on it was given up: never reused or synchronised
   hipStream_t stream = nullptr;
   std::vector<hipEvent_t> events;
   float* ws = nullptr;
@@ -63,13 +62,27 @@ struct StreamCtx {
   int probe_len = 0;
 };
 
-static std::vector<StreamCtx*> g_all;  // every context, for ct_shutdown
+static std::vector<StreamCtx*> g_pool;  // every context, for reuse and ct_shutdown
 
-struct ThreadState {
-  int generation = -1;
-  std::map<MaskKey, StreamCtx*> ctx;
+// A context held for the duration of a call (or of a tuning client).
+class Lease {
+ public:
+  Lease() = default;
+  Lease(const Lease&) = delete;
+  Lease& operator=(const Lease&) = delete;
+  ~Lease() { release(); }
+  StreamCtx* get() const { return c_; }
+  void set(StreamCtx* c) { c_ = c; }
+  void release() {
+    if (!c_) return;
+    std::lock_guard<std::mutex> g(g_mu);
+    c_->in_use = false;
+    c_ = nullptr;
+  }
+
+ private:
+  StreamCtx* c_ = nullptr;
 };
-static thread_local ThreadState t_state;
 
 static int check_init() {
   if (g_device < 0) {
@@ -111,22 +124,23 @@ static int make_key(const uint32_t* mask, int words, MaskKey* key) {
   return CT_OK;
 }
 
-// The calling thread's stream context for a mask (created on first use).
-static int get_ctx(const MaskKey& key, StreamCtx** out) {
+// Takes an idle context of the mask from the pool, or creates one.
+static int acquire(const MaskKey& key, Lease* lease) {
   int rc = check_init();
   if (rc) return rc;
   HIP_TRY(hipSetDevice(g_device));
-  const int gen = g_generation.load();
-  if (t_state.generation != gen) {
-    t_state.ctx.clear();
-    t_state.generation = gen;
-  }
-  auto it = t_state.ctx.find(key);
-  if (it != t_state.ctx.end()) {
-    *out = it->second;
-    return CT_OK;
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    for (StreamCtx* c : g_pool)
+      if (!c->in_use && !c->abandoned && c->key == key) {
+        c->in_use = true;
+        lease->set(c);
+        return CT_OK;
+      }
   }
   StreamCtx* c = new StreamCtx();
+  c->key = key;
+  c->in_use = true;
   hipError_t e = hipExtStreamCreateWithCUMask(&c->stream, (uint32_t)mask_words_needed(), key.data());
   if (e != hipSuccess) {
     delete c;
@@ -134,11 +148,17 @@ static int get_ctx(const MaskKey& key, StreamCtx** out) {
   }
   {
     std::lock_guard<std::mutex> g(g_mu);
-    g_all.push_back(c);
+    g_pool.push_back(c);
   }
-  t_state.ctx[key] = c;
-  *out = c;
+  lease->set(c);
   return CT_OK;
+}
+
+static int acquire_mask(const uint32_t* mask, int words, Lease* lease) {
+  MaskKey key;
+  int rc = check_init();
+  if (rc || (rc = make_key(mask, words, &key))) return rc;
+  return acquire(key, lease);
 }
 
 static int ensure_events(StreamCtx* c, size_t n) {
@@ -180,7 +200,8 @@ static int ensure_err(StreamCtx* c, int slots) {
   return CT_OK;
 }
 
-static void release_ctx(StreamCtx* c) {
+static void destroy_ctx(StreamCtx* c) {
+  if (c->abandoned) return;  // work may still be queued on it: leave it alone
   if (c->stream) hipStreamSynchronize(c->stream);
   for (hipEvent_t e : c->events) hipEventDestroy(e);
   if (c->ws) hipFree(c->ws);
@@ -190,8 +211,37 @@ static void release_ctx(StreamCtx* c) {
   delete c;
 }
 
-static double now_s() {
-  return std::chrono::duration<double>(std::chrono::steady_clock::now().time_since_epoch()).count();
+// ------------------------------------------------------------------ references
+using OpKey = std::array<int32_t, sizeof(ct_op) / sizeof(int32_t)>;
+struct RefBuf {
+  float* d = nullptr;
+  int64_t n = 0;
+  float tol = 0.f;
+};
+static std::map<OpKey, RefBuf> g_refs;
+
+static OpKey op_key(const ct_op& op) {
+  OpKey k;
+  std::memcpy(k.data(), &op, sizeof(ct_op));
+  return k;
+}
+
+// The reference a measurement checks against: the explicit one, else the op's
+// registered one, else none.
+static void resolve_ref(const OpX& x, const ct_verify* v, const float** ref, float* tol) {
+  *ref = nullptr;
+  *tol = 0.f;
+  if (v && v->y_ref) {
+    *ref = v->y_ref;
+    *tol = v->tol;
+    return;
+  }
+  std::lock_guard<std::mutex> g(g_mu);
+  auto it = g_refs.find(op_key(x.op));
+  if (it != g_refs.end() && it->second.n == x.ny) {
+    *ref = it->second.d;
+    *tol = it->second.tol;
+  }
 }
 
 // ------------------------------------------------------------------ launch
@@ -218,14 +268,83 @@ static float median_of(std::vector<float> v) {
   return (float)(((double)v[n / 2 - 1] + (double)v[n / 2]) / 2.0);
 }
 
+// ------------------------------------------------------------------ watchdog
+constexpr double kSlackS = 0.05;
+constexpr double kDrainMinS = 2.0;
+constexpr double kDrainMaxS = 60.0;
+
+// Events recorded on one stream since the last wait, in enqueue order.
+struct EventLog {
+  std::vector<hipEvent_t> ev;
+  std::vector<int32_t> runs;   // runs enqueued since the previous event
+  std::vector<int32_t> owner;  // candidate whose runs end at the event
+  int pending = 0;
+  void clear() {
+    ev.clear();
+    runs.clear();
+    owner.clear();
+    pending = 0;
+  }
+  void record(hipEvent_t e, hipStream_t st, int who) {
+    hipEventRecord(e, st);
+    ev.push_back(e);
+    runs.push_back(pending);
+    owner.push_back(who);
+    pending = 0;
+  }
+};
+
+// Waits for every event of the log with the watchdog. Returns CT_OK (and the
+// owner of a missed deadline in *late, -1 if none), CT_E_TIMEOUT when the
+// stream did not drain (the context is then abandoned), or CT_E_HIP.
+static int wait_events(StreamCtx* c, const EventLog& lg, double run_limit_s, int* late) {
+  *late = -1;
+  const int n = (int)lg.ev.size();
+  int spins = 0;
+  auto done = [&](int k) -> int {
+    const hipError_t e = hipEventQuery(lg.ev[k]);
+    if (e == hipSuccess) return 1;
+    if (e == hipErrorNotReady) return 0;
+    return hip_fail("hipEventQuery", e);
+  };
+  auto nap = [&]() {
+    if (++spins < 4000) {
+      std::this_thread::yield();
+    } else {
+      std::this_thread::sleep_for(std::chrono::microseconds(50));
+    }
+  };
+  int64_t total_runs = 0;
+  for (int32_t r : lg.runs) total_runs += r;
+  const double drain = std::min(kDrainMaxS, std::max(kDrainMinS, 4.0 * run_limit_s * (double)total_runs));
+  const WatchResult w = watch_events(n, lg.runs.data(), run_limit_s, kSlackS, drain, done, now_s, nap);
+  if (w.rc) return w.rc;
+  if (w.expired >= 0) *late = lg.owner[w.expired];
+  if (!w.drained) {
+    {
+      std::lock_guard<std::mutex> g(g_mu);
+      c->abandoned = true;
+    }
+    set_error("a candidate ran past its time limit and the stream did not drain within " + std::to_string(drain) +
+              " s; the stream is abandoned");
+    return CT_E_TIMEOUT;
+  }
+  return CT_OK;
+}
+
 // The profile step: time n candidates on one stream with protocol o.
+// skip (optional): candidates that are not measured (their lat/status are the
+// caller's). on_batch (optional): called with each group [i0, i1) once its
+// results are final; returning false stops the measurement (CT_E_STOPPED).
 static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c, const ct_measure_opts& o,
-                        const ct_verify* v, const void* xin, const void* w, void* y, float* lat,
-                        int32_t* status, float* rep) {
+                        const ct_verify* v, const void* xin, const void* w, void* y, float* lat, int32_t* status,
+                        float* rep, const uint8_t* skip = nullptr,
+                        const std::function<bool(int, int)>& on_batch = nullptr) {
   std::vector<Geom> geo(n);
   std::vector<char> live(n, 0);
   int64_t maxws = 0;
   for (int i = 0; i < n; ++i) {
+    if (skip && skip[i]) continue;
     lat[i] = INFINITY;
     status[i] = CT_S_INVALID;
     if (rep)
@@ -238,14 +357,19 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
   }
   int rc = ensure_ws(c, maxws);
   if (rc) return rc;
-  const bool verify = v && v->y_ref;
+  const float* ref = nullptr;
+  float tol = 0.f;
+  resolve_ref(x, v, &ref, &tol);
   const int batch = std::min(o.batch, std::max(n, 1));
-  if (verify && (rc = ensure_err(c, batch))) return rc;
+  if (ref && (rc = ensure_err(c, batch))) return rc;
   const int R = o.repeats, L = o.launches;
-  if ((rc = ensure_events(c, (size_t)2 * R * batch))) return rc;
+  if ((rc = ensure_events(c, (size_t)2 * R * batch + 1))) return rc;
   hipStream_t st = c->stream;
+  const double limit_s = (double)o.timeout_ms * 1e-3;
+  EventLog lg;
 
   auto run = [&](int i) -> bool {  // one run of candidate i; false on launch failure
+    ++lg.pending;
     if (launch_once(x, s[i], geo[i], xin, w, y, c->ws, st) != 0) {
       live[i] = 0;
       status[i] = CT_S_LAUNCH;
@@ -254,14 +378,20 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
     return true;
   };
   auto timed = [&](int i, int slot, int r) {
-    hipEventRecord(c->events[(size_t)2 * (slot * R + r)], st);
+    lg.record(c->events[(size_t)2 * (slot * R + r)], st, i);
     for (int l = 0; l < L && live[i]; ++l) run(i);
-    hipEventRecord(c->events[(size_t)2 * (slot * R + r) + 1], st);
+    lg.record(c->events[(size_t)2 * (slot * R + r) + 1], st, i);
+  };
+  // candidates left unmeasured when a call gives up on its stream
+  auto abandon_rest = [&](int from) {
+    for (int i = from; i < n; ++i)
+      if (live[i]) status[i] = CT_S_TIMEOUT;
   };
 
   std::vector<float> reps(R);
   for (int b0 = 0; b0 < n; b0 += batch) {
     const int b1 = std::min(n, b0 + batch);
+    lg.clear();
     for (int i = b0; i < b1; ++i)
       for (int k = 0; k < o.warmup && live[i]; ++k) run(i);
     if (o.interleave) {
@@ -273,7 +403,15 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
         if (live[i])
           for (int r = 0; r < R; ++r) timed(i, i - b0, r);
     }
-    HIP_TRY(hipStreamSynchronize(st));
+    int late = -1;
+    if (!lg.ev.empty()) {
+      rc = wait_events(c, lg, limit_s, &late);
+      if (rc == CT_E_TIMEOUT) {
+        if (late >= 0) status[late] = CT_S_TIMEOUT;
+        abandon_rest(b0);
+      }
+      if (rc) return rc;
+    }
     for (int i = b0; i < b1; ++i) {
       if (!live[i]) continue;
       for (int r = 0; r < R; ++r) {
@@ -284,31 +422,43 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
         if (rep) rep[(int64_t)i * R + r] = reps[r];
       }
       lat[i] = median_of(reps);
-      if (lat[i] > o.timeout_ms * 1000.0f) status[i] = CT_S_TIMEOUT;
+      if (i == late || lat[i] > o.timeout_ms * 1000.0f) status[i] = CT_S_TIMEOUT;
     }
-    if (verify) {
+    if (ref) {
       // Re-run every live candidate once more, each followed by its check, so
       // the compared output is the candidate's own whatever the timing order.
+      lg.clear();
       for (int i = b0; i < b1; ++i) {
         if (!live[i]) continue;
         if (!run(i)) continue;
-        if (launch_max_error((const float*)y, v->y_ref, x.ny, c->err + 2 * (i - b0), st) != 0)
+        if (launch_max_error((const float*)y, ref, x.ny, c->err + 2 * (i - b0), st) != 0)
           return hip_fail("verification launch", hipGetLastError());
       }
       std::vector<unsigned> h(2 * (size_t)(b1 - b0));
       HIP_TRY(hipMemcpyAsync(h.data(), c->err, sizeof(unsigned) * h.size(), hipMemcpyDeviceToHost, st));
-      HIP_TRY(hipStreamSynchronize(st));
+      lg.record(c->events[(size_t)2 * R * batch], st, -1);
+      int late2 = -1;
+      rc = wait_events(c, lg, limit_s, &late2);
+      if (rc == CT_E_TIMEOUT) abandon_rest(b0);
+      if (rc) return rc;
+      HIP_TRY(hipStreamSynchronize(st));  // the copy into pageable memory has landed
       for (int i = b0; i < b1; ++i) {
         if (!live[i] || status[i] != CT_S_OK) continue;
         float e, m;
         std::memcpy(&e, &h[2 * (i - b0)], 4);
         std::memcpy(&m, &h[2 * (i - b0) + 1], 4);
-        if (!(e <= v->tol * m)) status[i] = CT_S_WRONG_ANSWER;
+        if (!(e <= tol * m)) status[i] = CT_S_WRONG_ANSWER;
       }
     }
+    for (int i = b0; i < b1; ++i)
+      if (!(skip && skip[i]) && status[i] != CT_S_OK && status[i] != CT_S_TIMEOUT &&
+          status[i] != CT_S_WRONG_ANSWER)
+        lat[i] = INFINITY;
+    if (on_batch && !on_batch(b0, b1)) {
+      set_error("measurement stopped by its caller");
+      return CT_E_STOPPED;
+    }
   }
-  for (int i = 0; i < n; ++i)
-    if (status[i] != CT_S_OK && status[i] != CT_S_TIMEOUT && status[i] != CT_S_WRONG_ANSWER) lat[i] = INFINITY;
   return CT_OK;
 }
 
@@ -325,112 +475,64 @@ static int derive_checked(const ct_op* op, OpX* x) {
   return CT_OK;
 }
 
-// ------------------------------------------------------------------ clients
-static void pin_to_core(int core) {
-  if (core < 0 || core >= CPU_SETSIZE) return;
-  cpu_set_t set;
-  CPU_ZERO(&set);
-  CPU_SET(core, &set);
-  pthread_setaffinity_np(pthread_self(), sizeof(set), &set);  // best effort
-}
-
-static int tune_job(ct_tune_job* j, StreamCtx* c, const ct_measure_opts& o1, const ct_measure_opts& o2,
-                    float eps) {
+// ------------------------------------------------------------------ tuning
+// Stage 1 on all candidates, then stage 2 on the top_t and the tie rule.
+static int tune_job(ct_tune_job* j, StreamCtx* c, const ct_measure_opts& o1, const ct_measure_opts& o2, float eps,
+                    RecordSink* sink) {
   OpX x;
   int rc = derive_checked(&j->op, &x);
   if (rc) return rc;
-  if (!j->cands || j->n_cands < 0 || !j->lat1_us || !j->status1 || j->top_t < 1 || !j->top_pos ||
-      !j->lat2_us) {
-    set_error("tune job: bad arrays");
-    return CT_E_ARG;
-  }
   j->t_start_s = now_s();
   j->n_top = 0;
   j->winner_pos = -1;
   j->winner_lat_us = INFINITY;
-  rc = measure_impl(x, j->cands, j->n_cands, c, o1, &j->verify, j->x, j->w, j->y, j->lat1_us, j->status1,
-                    nullptr);
+  std::function<bool(int, int)> on_batch;
+  if (sink) on_batch = [&](int i0, int i1) { return sink->candidates(*j, i0, i1); };
+  rc = measure_impl(x, j->cands, j->n_cands, c, o1, &j->verify, j->x, j->w, j->y, j->lat1_us, j->status1, nullptr,
+                    j->skip, on_batch);
   if (rc) return rc;
-  int32_t n_top = 0;
-  rc = ct_top_t(j->lat1_us, j->status1, j->n_cands, j->top_t, j->top_pos, &n_top);
-  if (rc) return rc;
-  j->n_top = n_top;
-  if (n_top > 0) {
-    std::vector<ct_schedule> s2(n_top);
-    for (int i = 0; i < n_top; ++i) s2[i] = j->cands[j->top_pos[i]];
-    std::vector<int32_t> st2(n_top);
-    ct_measure_opts o = o2;
-    o.interleave = 1;
-    rc = measure_impl(x, s2.data(), n_top, c, o, nullptr, j->x, j->w, j->y, j->lat2_us, st2.data(), nullptr);
-    if (rc) return rc;
-    for (int i = 0; i < n_top; ++i)
-      if (st2[i] != CT_S_OK) j->lat2_us[i] = INFINITY;
-    int32_t wi = -1;
-    rc = ct_select_winner(j->lat2_us, j->top_pos, n_top, eps, &wi);
-    if (rc) return rc;
-    if (wi >= 0) {
-      j->winner_pos = j->top_pos[wi];
-      j->winner_lat_us = j->lat2_us[wi];
-    }
-  }
+  ct_measure_opts o = o2;
+  o.interleave = 1;
+  rc = select_job(j, eps, [&](const int32_t* pos, int nt, float* lat2) {
+    std::vector<ct_schedule> s2(nt);
+    for (int i = 0; i < nt; ++i) s2[i] = j->cands[pos[i]];
+    std::vector<int32_t> st2(nt);
+    int r = measure_impl(x, s2.data(), nt, c, o, nullptr, j->x, j->w, j->y, lat2, st2.data(), nullptr);
+    if (r) return r;
+    for (int i = 0; i < nt; ++i)
+      if (st2[i] != CT_S_OK) lat2[i] = INFINITY;
+    return CT_OK;
+  });
   j->t_end_s = now_s();
-  return CT_OK;
+  return rc;
 }
 
-// The jobs a client runs: its own list in order, or (next != nullptr) the
-// next unclaimed job of a queue shared by all clients.
-struct JobSource {
-  ct_tune_job* jobs;
-  int n;
-  std::atomic<int>* next;
-  int32_t* owner;  // shared queue: owner[i] = index of the client that ran job i
-};
-
-static void run_client(ct_client* cl, int index, JobSource src, const ct_measure_opts* o1,
-                       const ct_measure_opts* o2, float eps) {
-  pin_to_core(cl->host_core);
-  cl->rc = CT_OK;
-  cl->n_measured = 0;
-  cl->t_start_s = now_s();
-  cl->t_end_s = cl->t_start_s;
-  try {
-    MaskKey key;
-    int rc = make_key(cl->cu_mask, CT_MASK_WORDS, &key);
-    StreamCtx* c = nullptr;
-    if (!rc) rc = get_ctx(key, &c);
-    // CT_PROGRESS set in the environment: one line on stderr per finished job
-    const bool progress = getenv("CT_PROGRESS") != nullptr;
-    for (int k = 0; !rc; ++k) {
-      int i = k;
-      if (src.next) i = src.next->fetch_add(1);
-      if (i >= src.n) break;
-      if (src.owner) src.owner[i] = index;
-      rc = tune_job(&src.jobs[i], c, *o1, *o2, eps);
-      if (!rc) cl->n_measured += src.jobs[i].n_cands;
-      if (progress)
-        fprintf(stderr, "[ct] client %d: job %d of %d done, rc %d, %.1f s\n", index, i + 1, src.n, rc,
-                now_s() - cl->t_start_s);
+static int check_jobs(const ct_tune_job* jobs, int n_jobs) {
+  for (int i = 0; i < n_jobs; ++i) {
+    const ct_tune_job& j = jobs[i];
+    if (!j.cands || j.n_cands < 0 || !j.lat1_us || !j.status1 || j.top_t < 1 || !j.top_pos || !j.lat2_us ||
+        !j.x || !j.w || !j.y) {
+      set_error("tune job " + std::to_string(i) + ": bad arrays");
+      return CT_E_ARG;
     }
-    cl->rc = rc;
-  } catch (...) {
-    set_error("tuning client: unexpected exception");
-    cl->rc = CT_E_ARG;
   }
-  cl->t_end_s = now_s();
+  return CT_OK;
 }
 
-static int run_clients(ct_client* clients, int n_clients, const std::vector<JobSource>& src,
-                       const ct_measure_opts* stage1, const ct_measure_opts* stage2, float eps) {
-  std::vector<std::thread> th;
-  th.reserve(n_clients);
-  for (int i = 0; i < n_clients; ++i) th.emplace_back(run_client, &clients[i], i, src[i], stage1, stage2, eps);
-  for (auto& t : th) t.join();
-  for (int i = 0; i < n_clients; ++i)
-    if (clients[i].rc) {
-      set_error("tuning client " + std::to_string(i) + " failed with code " + std::to_string(clients[i].rc));
-      return clients[i].rc;
+// Runs the clients on the device: each holds one context of its mask for all
+// of its jobs.
+static int run_device_clients(ct_client* clients, int n_clients, const std::vector<JobSource>& src,
+                              const ct_measure_opts* o1, const ct_measure_opts* o2, float eps) {
+  std::vector<Lease> leases(n_clients);  // slot i is touched by client thread i only
+  JobFn fn = [&](int ci, ct_tune_job* j, RecordSink* sink) -> int {
+    if (!leases[ci].get()) {
+      const int rc = acquire_mask(clients[ci].cu_mask, CT_MASK_WORDS, &leases[ci]);
+      if (rc) return rc;
     }
-  return CT_OK;
+    return tune_job(j, leases[ci].get(), *o1, *o2, eps, sink);
+  };
+  ClientEndFn end = [&](int ci) { leases[ci].release(); };
+  return run_clients(clients, n_clients, src, fn, end, -1);
 }
 
 }  // namespace ct
@@ -439,8 +541,6 @@ static int run_clients(ct_client* clients, int n_clients, const std::vector<JobS
 using namespace ct;
 
 extern "C" {
-
-const char* ct_last_error(void) { return t_err.c_str(); }
 
 int ct_init(int device) {
   std::lock_guard<std::mutex> g(g_mu);
@@ -482,18 +582,59 @@ int ct_num_cus(void) {
 
 void ct_shutdown(void) {
   std::lock_guard<std::mutex> g(g_mu);
+  if (g_device < 0 && g_pool.empty() && g_refs.empty()) return;  // nothing to release (a second call)
   if (g_device >= 0) hipSetDevice(g_device);
-  for (StreamCtx* c : g_all) release_ctx(c);
-  g_all.clear();
-  g_generation.fetch_add(1);
+  for (StreamCtx* c : g_pool) destroy_ctx(c);
+  g_pool.clear();
+  for (auto& kv : g_refs) hipFree(kv.second.d);
+  g_refs.clear();
   g_device = -1;
   g_num_cus = 0;
+}
+
+int ct_stream_count(void) {
+  std::lock_guard<std::mutex> g(g_mu);
+  return (int)g_pool.size();
 }
 
 int ct_cu_mask(double fraction, int slot, uint32_t* mask, int words) {
   int rc = check_init();
   if (rc) return rc;
   return ct_build_cu_mask(g_num_cus, fraction, slot, mask, words);
+}
+
+int ct_set_reference(const ct_op* op, const double* y_ref_host) {
+  OpX ox;
+  int rc = derive_checked(op, &ox);
+  if (rc || (rc = check_init())) return rc;
+  const OpKey key = op_key(*op);
+  float* d = nullptr;
+  if (y_ref_host) {
+    std::vector<float> h((size_t)ox.ny);
+    for (int64_t i = 0; i < ox.ny; ++i) h[(size_t)i] = (float)y_ref_host[i];
+    HIP_TRY(hipSetDevice(g_device));
+    if (hipMalloc((void**)&d, sizeof(float) * (size_t)ox.ny) != hipSuccess) {
+      set_error("ct_set_reference: allocation failed");
+      return CT_E_OOM;
+    }
+    const hipError_t e = hipMemcpy(d, h.data(), sizeof(float) * (size_t)ox.ny, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      hipFree(d);
+      return hip_fail("ct_set_reference: upload", e);
+    }
+  }
+  float* old = nullptr;
+  {
+    std::lock_guard<std::mutex> g(g_mu);
+    auto it = g_refs.find(key);
+    if (it != g_refs.end()) {
+      old = it->second.d;
+      g_refs.erase(it);
+    }
+    if (d) g_refs[key] = RefBuf{d, ox.ny, op->dtype == CT_DT_BF16 ? 2e-2f : 1e-4f};
+  }
+  if (old) HIP_TRY(hipFree(old));
+  return CT_OK;
 }
 
 int conv2d_run(const ct_op* op, const ct_schedule* s, const void* x, const void* w, void* y,
@@ -511,10 +652,9 @@ int conv2d_run(const ct_op* op, const ct_schedule* s, const void* x, const void*
     set_error("conv2d_run: invalid schedule: " + why);
     return CT_E_ARG;
   }
-  MaskKey key;
-  if ((rc = check_init()) || (rc = make_key(cu_mask, words, &key))) return rc;
-  StreamCtx* c = nullptr;
-  if ((rc = get_ctx(key, &c))) return rc;
+  Lease lease;
+  if ((rc = acquire_mask(cu_mask, words, &lease))) return rc;
+  StreamCtx* c = lease.get();
   if ((rc = ensure_ws(c, g.ws_floats))) return rc;
   const int lrc = launch_once(ox, *s, g, x, w, y, c->ws, c->stream);
   if (lrc == -2) return CT_E_ARG;  // the launcher refused the arguments (reason already set)
@@ -533,11 +673,9 @@ int measure_candidates_mask(const ct_op* op, const ct_schedule* s, int n, const 
     set_error("measure_candidates: bad argument");
     return CT_E_ARG;
   }
-  MaskKey key;
-  if ((rc = check_init()) || (rc = make_key(cu_mask, words, &key))) return rc;
-  StreamCtx* c = nullptr;
-  if ((rc = get_ctx(key, &c))) return rc;
-  return measure_impl(ox, s, n, c, *o, v, x, w, y, lat_us, status, rep_us);
+  Lease lease;
+  if ((rc = acquire_mask(cu_mask, words, &lease))) return rc;
+  return measure_impl(ox, s, n, lease.get(), *o, v, x, w, y, lat_us, status, rep_us);
 }
 
 int measure_candidates(const ct_op* op, const ct_schedule* s, int n, double cu_fraction,
@@ -559,8 +697,15 @@ int ct_tune_clients(ct_client* clients, int n_clients, const ct_measure_opts* st
     return CT_E_ARG;
   }
   std::vector<JobSource> src(n_clients);
-  for (int i = 0; i < n_clients; ++i) src[i] = {clients[i].jobs, clients[i].n_jobs, nullptr, nullptr};
-  return run_clients(clients, n_clients, src, stage1, stage2, eps);
+  for (int i = 0; i < n_clients; ++i) {
+    if (clients[i].n_jobs < 0 || (clients[i].n_jobs > 0 && !clients[i].jobs) ||
+        (rc = check_jobs(clients[i].jobs, clients[i].n_jobs))) {
+      if (!rc) set_error("ct_tune_clients: bad job list");
+      return rc ? rc : CT_E_ARG;
+    }
+    src[i] = {clients[i].jobs, clients[i].n_jobs, nullptr, nullptr};
+  }
+  return run_device_clients(clients, n_clients, src, stage1, stage2, eps);
 }
 
 int ct_tune_shared(ct_client* clients, int n_clients, ct_tune_job* jobs, int n_jobs,
@@ -573,11 +718,76 @@ int ct_tune_shared(ct_client* clients, int n_clients, ct_tune_job* jobs, int n_j
     set_error("ct_tune_shared: bad argument");
     return CT_E_ARG;
   }
+  if ((rc = check_jobs(jobs, n_jobs))) return rc;
   if (job_client)
     for (int i = 0; i < n_jobs; ++i) job_client[i] = -1;
   std::atomic<int> next{0};
   std::vector<JobSource> src(n_clients, JobSource{jobs, n_jobs, &next, job_client});
-  return run_clients(clients, n_clients, src, stage1, stage2, eps);
+  return run_device_clients(clients, n_clients, src, stage1, stage2, eps);
+}
+
+int ct_tune_split(ct_tune_job* job, const uint32_t* masks, int k, int words, void* const* y_slots,
+                  const ct_measure_opts* stage1, const ct_measure_opts* stage2, float eps, double* screen_s) {
+  int rc = check_init();
+  if (rc) return rc;
+  if (!job || !masks || k < 1 || k > 64 || !y_slots || !opts_ok(stage1) || !opts_ok(stage2) || !(eps >= 0.f)) {
+    set_error("ct_tune_split: bad argument");
+    return CT_E_ARG;
+  }
+  for (int j = 0; j < k; ++j)
+    if (!y_slots[j]) {
+      set_error("ct_tune_split: null output buffer");
+      return CT_E_ARG;
+    }
+  if ((rc = check_jobs(job, 1))) return rc;
+  OpX x;
+  if ((rc = derive_checked(&job->op, &x))) return rc;
+  job->t_start_s = now_s();
+  job->n_top = 0;
+  job->winner_pos = -1;
+  job->winner_lat_us = INFINITY;
+  const int n = job->n_cands;
+  std::vector<int> rcs(k, CT_OK);
+  std::vector<std::string> errs(k);
+  auto screen = [&](int j) {
+    const int b = (int)((int64_t)n * j / k), e = (int)((int64_t)n * (j + 1) / k);
+    Lease lease;
+    int r = acquire_mask(masks + (size_t)j * words, words, &lease);
+    if (!r && e > b)
+      r = measure_impl(x, job->cands + b, e - b, lease.get(), *stage1, &job->verify, job->x, job->w, y_slots[j],
+                       job->lat1_us + b, job->status1 + b, nullptr, job->skip ? job->skip + b : nullptr);
+    rcs[j] = r;
+    if (r) errs[j] = last_error();
+  };
+  const double t0 = now_s();
+  {
+    std::vector<std::thread> th;
+    for (int j = 0; j < k; ++j) th.emplace_back(screen, j);
+    for (auto& t : th) t.join();
+  }
+  if (screen_s) *screen_s = now_s() - t0;
+  for (int j = 0; j < k; ++j)
+    if (rcs[j]) {
+      set_error("ct_tune_split: slot " + std::to_string(j) + ": " + errs[j]);
+      return job->rc = rcs[j];
+    }
+  Lease lease0;
+  if ((rc = acquire_mask(masks, words, &lease0))) return job->rc = rc;
+  ct_measure_opts o2 = *stage2;
+  o2.interleave = 1;
+  rc = select_job(job, eps, [&](const int32_t* pos, int nt, float* lat2) {
+    std::vector<ct_schedule> s2(nt);
+    for (int i = 0; i < nt; ++i) s2[i] = job->cands[pos[i]];
+    std::vector<int32_t> st2(nt);
+    int r = measure_impl(x, s2.data(), nt, lease0.get(), o2, nullptr, job->x, job->w, y_slots[0], lat2, st2.data(),
+                         nullptr);
+    if (r) return r;
+    for (int i = 0; i < nt; ++i)
+      if (st2[i] != CT_S_OK) lat2[i] = INFINITY;
+    return CT_OK;
+  });
+  job->t_end_s = now_s();
+  return job->rc = rc;
 }
 
 int ct_cross_eval(const ct_op* op, const ct_schedule* s, int n_sched, const uint32_t* masks, int n_masks,
@@ -595,11 +805,10 @@ int ct_cross_eval(const ct_op* op, const ct_schedule* s, int n_sched, const uint
   std::vector<float> lat(n_sched);
   std::vector<int32_t> st(n_sched);
   for (int j = 0; j < n_masks; ++j) {
-    MaskKey key;
-    if ((rc = make_key(masks + (size_t)j * words, words, &key))) return rc;
-    StreamCtx* c = nullptr;
-    if ((rc = get_ctx(key, &c))) return rc;
-    if ((rc = measure_impl(ox, s, n_sched, c, oo, nullptr, x, w, y, lat.data(), st.data(), nullptr))) return rc;
+    Lease lease;
+    if ((rc = acquire_mask(masks + (size_t)j * words, words, &lease))) return rc;
+    if ((rc = measure_impl(ox, s, n_sched, lease.get(), oo, nullptr, x, w, y, lat.data(), st.data(), nullptr)))
+      return rc;
     for (int i = 0; i < n_sched; ++i) M[(size_t)i * n_masks + j] = st[i] == CT_S_OK ? lat[i] : INFINITY;
   }
   return CT_OK;
@@ -607,14 +816,13 @@ int ct_cross_eval(const ct_op* op, const ct_schedule* s, int n_sched, const uint
 
 int ct_probe_cus(const uint32_t* cu_mask, int words, int blocks, int32_t* out, int cap, int32_t* n_out) {
   int rc;
-  MaskKey key;
   if (blocks < 1 || blocks > (1 << 20) || !n_out) {
     set_error("ct_probe_cus: bad argument");
     return CT_E_ARG;
   }
-  if ((rc = check_init()) || (rc = make_key(cu_mask, words, &key))) return rc;
-  StreamCtx* c = nullptr;
-  if ((rc = get_ctx(key, &c))) return rc;
+  Lease lease;
+  if ((rc = acquire_mask(cu_mask, words, &lease))) return rc;
+  StreamCtx* c = lease.get();
   if (c->probe_len < blocks) {
     if (c->probe) HIP_TRY(hipFree(c->probe));
     c->probe = nullptr;
@@ -636,14 +844,13 @@ int ct_probe_cus(const uint32_t* cu_mask, int words, int blocks, int32_t* out, i
 static int probe_timed(const uint32_t* cu_mask, int words, const ct_measure_opts* o, float* us,
                        const std::function<int(hipStream_t)>& body) {
   int rc;
-  MaskKey key;
   if (!opts_ok(o) || !us) {
     set_error("probe: bad argument");
     return CT_E_ARG;
   }
-  if ((rc = check_init()) || (rc = make_key(cu_mask, words, &key))) return rc;
-  StreamCtx* c = nullptr;
-  if ((rc = get_ctx(key, &c))) return rc;
+  Lease lease;
+  if ((rc = acquire_mask(cu_mask, words, &lease))) return rc;
+  StreamCtx* c = lease.get();
   if ((rc = ensure_events(c, (size_t)2 * o->repeats))) return rc;
   for (int k = 0; k < o->warmup; ++k)
     if (body(c->stream)) return hip_fail("probe launch", hipGetLastError());

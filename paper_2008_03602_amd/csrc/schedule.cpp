@@ -589,6 +589,25 @@ static int valid_space(const ct_op* op, std::vector<ct_schedule>* out) {
   return CT_OK;
 }
 
+int ct_grid_size(const ct_op* op, int family, int64_t* n) {
+  if (!op || !n) { set_error("ct_grid_size: null argument"); return CT_E_ARG; }
+  const FamilyDef* f = family_def(family);
+  if (!f) { set_error("ct_grid_size: unknown family"); return CT_E_ARG; }
+  OpX x;
+  std::string why;
+  if (!derive_op(*op, &x, &why)) { set_error(why); return CT_E_ARG; }
+  *n = 0;
+  if (!family_applies(family, x)) return CT_OK;
+  const int64_t size = family_grid_size(*f);
+  ct_schedule s;
+  Geom g;
+  for (int64_t i = 0; i < size; ++i) {
+    ct_grid_decode(family, i, &s);
+    if (compute_geom(x, s, &g, nullptr) == CT_OK) ++*n;
+  }
+  return CT_OK;
+}
+
 int ct_valid_space(const ct_op* op, ct_schedule* out, int64_t cap, int64_t* count) {
   if (!op || !count) { set_error("ct_valid_space: null argument"); return CT_E_ARG; }
   std::vector<ct_schedule> v;

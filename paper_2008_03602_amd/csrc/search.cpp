@@ -357,10 +357,6 @@ bool opts_ok(const ct_search_opts* so) {
          so->explore >= 0.0f && so->explore <= 1.0f && so->eps >= 0.0f && so->sa_temp >= 0.0f && so->cus >= 0;
 }
 
-double now_s() {
-  return std::chrono::duration<double>(std::chrono::steady_clock::now().time_since_epoch()).count();
-}
-
 }  // namespace
 }  // namespace ct
 

@@ -82,48 +82,22 @@ class Slots:
 
 
 def split_screen(ld: T.LayerData, cands: List[L.ct_schedule], cfg: W.TuneConfig, fraction: float, k: int,
-                 slots: Slots, ys: Sequence[torch.Tensor]) -> dict:
-    """Screen cands on slots 0..k-1 of `fraction` at once (contiguous parts of
-    the sample), then re-measure the global top T on slot 0 and select."""
-    n = len(cands)
-    parts = [list(range(n * j // k, n * (j + 1) // k)) for j in range(k)]
-    lat1 = np.full(n, np.inf, dtype=np.float32)
-    st1 = np.zeros(n, dtype=np.int32)
-    o1 = L.opts_from_protocol(cfg.stage1)
-
-    def screen(j: int):
-        idx = parts[j]
-        if idx:
-            return L.measure_candidates_mask(ld.op, [cands[i] for i in idx], L.ct_cu_mask(fraction, j), o1,
-                                             ld.x, ld.w, ys[j])
-        return None
-
-    t0 = time.perf_counter()
-    futs = [slots.submit(j, lambda j=j: screen(j)) for j in range(k)]
-    for j, f in enumerate(futs):
-        r = f.result()
-        if r is not None:
-            lat1[parts[j]] = r[0]
-            st1[parts[j]] = r[1]
-    t_screen = time.perf_counter() - t0
-    top = L.ct_top_t(lat1, st1, cfg.top_t)
-    o2 = L.opts_from_protocol(cfg.stage2, batch=len(top), interleave=1)
-    lat2, st2 = slots.submit(0, lambda: L.measure_candidates_mask(
-        ld.op, [cands[i] for i in top], L.ct_cu_mask(fraction, 0), o2, ld.x, ld.w, ys[0])).result()
-    lat2 = np.where(st2 == L.S_OK, lat2, np.inf).astype(np.float32)
-    pos = np.asarray(top, dtype=np.int32)
-    wi = L.ct_select_winner(lat2, pos, cfg.eps) if len(pos) else -1
-    t_total = time.perf_counter() - t0
-    return {"k": k, "screen_s": t_screen, "total_s": t_total, "screened_ok": int(np.sum(st1 == L.S_OK)),
-            "winner_pos": int(pos[wi]) if wi >= 0 else -1,
-            "winner_lat_us": float(lat2[wi]) if wi >= 0 else float("inf")}
+                 slots: "Slots", ys: Sequence[torch.Tensor], y_ref=None) -> dict:
+    """One client over k CU slots (ct_tune_split runs the k screens at once,
+    the merge, the re-measure on slot 0 and the selection). Runs on slot 0's
+    thread so that the study's threads stay one per slot."""
+    r = slots.submit(0, lambda: T.tune_split(ld, cands, cfg, fraction, k, ys, y_ref=y_ref)).result()
+    r.pop("result")
+    return r
 
 
 def tsi_scaling(layers: Sequence[T.LayerData], cands: Dict[int, List[L.ct_schedule]], cfg: W.TuneConfig,
-                fraction: float = 0.25, ks: Sequence[int] = (1, 2, 4)) -> dict:
+                fraction: float = 0.25, ks: Sequence[int] = (1, 2, 4), verify_refs=None) -> dict:
     """Per layer and k: tuning time with the candidate list spread over k
     slots of `fraction`. Where a winner differs from the k = 1 winner, the two
-    are re-timed side by side on slot 0 and their relative gap reported."""
+    are re-timed side by side on slot 0 and their relative gap reported.
+    verify_refs (optional, per layer id): fp32 device references that every
+    screened candidate of every slot is checked against."""
     kmax = max(ks)
     out = {"fraction": fraction, "ks": list(ks), "layers": []}
     with Slots(kmax) as slots:
@@ -142,7 +116,8 @@ def tsi_scaling(layers: Sequence[T.LayerData], cands: Dict[int, List[L.ct_schedu
             row = {"layer": ld.op.name, "candidates": len(c), "runs": []}
             base = None
             for k in ks:
-                r = split_screen(ld, c, cfg, fraction, k, slots, ys[ld.layer_id])
+                r = split_screen(ld, c, cfg, fraction, k, slots, ys[ld.layer_id],
+                                 (verify_refs or {}).get(ld.layer_id))
                 if base is None:
                     base = r
                 elif r["winner_pos"] != base["winner_pos"] and r["winner_pos"] >= 0 and base["winner_pos"] >= 0:
@@ -167,19 +142,24 @@ def tsi_scaling(layers: Sequence[T.LayerData], cands: Dict[int, List[L.ct_schedu
 
 
 def isolation(ld: T.LayerData, scheds: List[L.ct_schedule], cfg: W.TuneConfig, slots: Slots,
-              copy_bufs: Sequence, ys: Sequence[torch.Tensor]) -> dict:
+              copy_bufs: Sequence, ys: Sequence[torch.Tensor], y_ref=None) -> dict:
     """Stage-2 latencies of fixed schedules on slot 0 of the 25 % share alone,
     with slots 1-3 running the same kernels, with slots 1-3 copying, and on
-    an unmasked stream alone and with slots 1-3 running the same kernels."""
+    an unmasked stream alone and with slots 1-3 running the same kernels.
+    y_ref (optional): fp32 device reference that every timed schedule's output
+    is checked against in every condition (statuses in "status")."""
     o = L.opts_from_protocol(cfg.stage2, batch=len(scheds), interleave=1)
     bg_opts = L.make_opts(0, 1, 10, len(scheds))
     copy_opts = L.make_opts(0, 1, 1, 1)
+    statuses = {}
 
-    def timed(mask):
-        lat, st = slots.submit(0, lambda: L.measure_candidates_mask(ld.op, scheds, mask, o, ld.x, ld.w, ys[0])).result()
+    def timed(mask, key):
+        lat, st = slots.submit(0, lambda: L.measure_candidates_mask(ld.op, scheds, mask, o, ld.x, ld.w, ys[0],
+                                                                    y_ref=y_ref, tol=1e-4)).result()
+        statuses[key] = st.tolist()
         return np.where(st == L.S_OK, lat, np.inf).astype(np.float64)
 
-    def with_load(kind: str, mask) -> np.ndarray:
+    def with_load(kind: str, mask, key: str) -> np.ndarray:
         stop = threading.Event()
 
         def loop(j: int):
@@ -197,7 +177,7 @@ def isolation(ld: T.LayerData, scheds: List[L.ct_schedule], cfg: W.TuneConfig, s
         futs = [slots.submit(j, lambda j=j: loop(j)) for j in (1, 2, 3)]
         time.sleep(0.05)  # the load is running before the timing starts
         try:
-            return timed(mask)
+            return timed(mask, key)
         finally:
             stop.set()
             for f in futs:
@@ -206,12 +186,13 @@ def isolation(ld: T.LayerData, scheds: List[L.ct_schedule], cfg: W.TuneConfig, s
     mask0 = L.ct_cu_mask(0.25, 0)
     full = L.ct_cu_mask(1.0, 0)
     res = {"layer": ld.op.name, "schedules": [T.describe_schedule(ld.op, s)["knobs"] for s in scheds]}
-    lat = {"alone": timed(mask0),
-           "neighbours_same_kernels": with_load("same", mask0),
-           "neighbours_copying": with_load("copy", mask0),
-           "unmasked_alone": timed(full),
-           "unmasked_shared": with_load("same", full)}
+    lat = {"alone": timed(mask0, "alone"),
+           "neighbours_same_kernels": with_load("same", mask0, "neighbours_same_kernels"),
+           "neighbours_copying": with_load("copy", mask0, "neighbours_copying"),
+           "unmasked_alone": timed(full, "unmasked_alone"),
+           "unmasked_shared": with_load("same", full, "unmasked_shared")}
     res["latency_us"] = {k: v.tolist() for k, v in lat.items()}
+    res["status"] = statuses
     res["inflation"] = {
         "neighbours_same_kernels": (lat["neighbours_same_kernels"] / lat["alone"]).tolist(),
         "neighbours_copying": (lat["neighbours_copying"] / lat["alone"]).tolist(),

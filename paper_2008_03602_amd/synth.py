@@ -42,13 +42,25 @@ def splitmix64_block(state0: int, count: int, skip: int = 1) -> np.ndarray:
     The k-th call (k = 1, 2, ...) mixes state0 + k*GAMMA, so any window of the
     stream can be produced without a loop.
     """
-    k = np.arange(skip + 1, skip + 1 + count, dtype=np.uint64)
+    out = np.empty(count, dtype=np.uint64)
+    chunk = 1 << 20  # in place, a chunk at a time: large tensors stay cache- and memory-friendly
+    t = np.empty(min(chunk, max(count, 1)), dtype=np.uint64)
     with np.errstate(over="ignore"):
-        z = np.uint64(state0) + k * np.uint64(GAMMA)
-        z = (z ^ (z >> np.uint64(30))) * np.uint64(_M1)
-        z = (z ^ (z >> np.uint64(27))) * np.uint64(_M2)
-        z = z ^ (z >> np.uint64(31))
-    return z
+        for b in range(0, count, chunk):
+            z = out[b:b + chunk]
+            tt = t[:len(z)]
+            z[:] = np.arange(skip + 1 + b, skip + 1 + b + len(z), dtype=np.uint64)
+            z *= np.uint64(GAMMA)
+            z += np.uint64(state0)
+            np.right_shift(z, np.uint64(30), out=tt)
+            z ^= tt
+            z *= np.uint64(_M1)
+            np.right_shift(z, np.uint64(27), out=tt)
+            z ^= tt
+            z *= np.uint64(_M2)
+            np.right_shift(z, np.uint64(31), out=tt)
+            z ^= tt
+    return out
 
 
 def _unit(z: np.ndarray) -> np.ndarray:
@@ -61,7 +73,12 @@ def draw(shape, dist: str, seed: int, config_id: int, tag: int, layer_id: int,
     count = int(np.prod(shape))
     s0 = stream_state(seed, config_id, tag, layer_id)
     if dist == "uniform":
-        v = 2.0 * _unit(splitmix64_block(s0, count)) - 1.0
+        z = splitmix64_block(s0, count)
+        z >>= np.uint64(11)
+        v = z.astype(np.float64)
+        del z
+        v *= 2.0 ** -52  # 2 * (z >> 11) * 2^-53, exact
+        v -= 1.0
     elif dist == "normal":
         z = splitmix64_block(s0, 2 * count)
         u1 = _unit(z[0::2])

@@ -117,26 +117,44 @@ class _Keep:
         return x
 
 
-def _fill_job(jb, ld: LayerData, c: List[L.ct_schedule], cfg: W.TuneConfig, keep: _Keep,
-              verify_refs: Optional[Dict[int, torch.Tensor]], verify_tol: float):
-    """Point one ct_tune_job at a layer's buffers, candidates and result arrays."""
+def fill_job(jb, op: W.Op, layer_id: int, x, w, y, c: List[L.ct_schedule], top_t: int, keep: _Keep,
+             y_ref: Optional[torch.Tensor] = None, verify_tol: float = 1e-4, recorded: Optional[dict] = None):
+    """Point one ct_tune_job at a layer's buffers, candidates and result arrays.
+    recorded (resume): {sample position: (lat_us, status)} of candidates that a
+    log already holds; they are passed as skipped, with their recorded values."""
     arr = keep.add(L.schedule_array(c))
     n = len(c)
     lat1 = keep.add(np.zeros(max(n, 1), np.float32))
     st1 = keep.add(np.zeros(max(n, 1), np.int32))
-    top = keep.add(np.zeros(cfg.top_t, np.int32))
-    lat2 = keep.add(np.zeros(cfg.top_t, np.float32))
-    jb.op = L.make_op(ld.op)
-    jb.x, jb.w, jb.y = ld.x.data_ptr(), ld.w.data_ptr(), ld.y.data_ptr()
+    top = keep.add(np.zeros(top_t, np.int32))
+    lat2 = keep.add(np.zeros(top_t, np.float32))
+    jb.op = L.make_op(op)
+    jb.x, jb.w, jb.y = L._ptr(x), L._ptr(w), L._ptr(y)
     jb.cands, jb.n_cands = arr, n
-    if verify_refs is not None and ld.layer_id in verify_refs:
-        jb.verify = L.ct_verify(verify_refs[ld.layer_id].data_ptr(), verify_tol)
+    jb.layer_id = layer_id
+    if y_ref is not None:
+        jb.verify = L.ct_verify(y_ref.data_ptr(), verify_tol)
+    if recorded:
+        skip = keep.add(np.zeros(max(n, 1), np.uint8))
+        for pos, (lat, st) in recorded.items():
+            if 0 <= pos < n:
+                skip[pos] = 1
+                lat1[pos] = np.float32(lat)
+                st1[pos] = st
+        jb.skip = skip.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))
     jb.lat1_us = lat1.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
     jb.status1 = st1.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
-    jb.top_t = cfg.top_t
+    jb.top_t = top_t
     jb.top_pos = top.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
     jb.lat2_us = lat2.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
-    return (ld, c, lat1, st1, top, lat2)
+    return (c, lat1, st1, top, lat2)
+
+
+def _fill_job(jb, ld: LayerData, c: List[L.ct_schedule], cfg: W.TuneConfig, keep: _Keep,
+              verify_refs: Optional[Dict[int, torch.Tensor]], verify_tol: float, recorded=None):
+    ref = verify_refs.get(ld.layer_id) if verify_refs is not None else None
+    return (ld,) + fill_job(jb, ld.op, ld.layer_id, ld.x, ld.w, ld.y, c, cfg.top_t, keep, ref, verify_tol,
+                            recorded)
 
 
 def _result(jb, meta, client: int, fraction: float) -> JobResult:
@@ -146,13 +164,32 @@ def _result(jb, meta, client: int, fraction: float) -> JobResult:
                      top[:nt].copy(), lat2[:nt].copy(), jb.winner_pos, jb.winner_lat_us, jb.t_start_s, jb.t_end_s)
 
 
-def _clients(masks: Sequence[np.ndarray], pin_cores: bool) -> ctypes.Array:
+def _clients(masks: Sequence[np.ndarray], pin_cores: bool, log_paths: Optional[Sequence[str]] = None,
+             keep: Optional[_Keep] = None) -> ctypes.Array:
     clients = (L.ct_client * len(masks))()
     for j, m in enumerate(masks):
         for k, v in enumerate(m):
             clients[j].cu_mask[k] = int(v)
         clients[j].host_core = j if pin_cores else -1
+        if log_paths is not None:
+            b = log_paths[j].encode()
+            if keep is not None:
+                keep.add(b)
+            clients[j].log_path = b
     return clients
+
+
+@dataclass
+class ClientStats:
+    """What the library reports per client after a run."""
+    n_measured: int
+    t_start: float
+    t_end: float
+    cands_per_s: float
+
+
+def client_stats(clients: ctypes.Array) -> List[ClientStats]:
+    return [ClientStats(int(c.n_measured), c.t_start_s, c.t_end_s, c.cands_per_s) for c in clients]
 
 
 def tune_clients(assignments: Sequence[Sequence[LayerData]], masks: Sequence[np.ndarray],
@@ -183,21 +220,57 @@ def tune_clients(assignments: Sequence[Sequence[LayerData]], masks: Sequence[np.
     return out
 
 
+class SharedRun(list):
+    """JobResults of one shared-queue run, plus the library's client figures."""
+    clients: List[ClientStats]
+    cands_per_s: float
+
+
 def tune_shared(layers: Sequence[LayerData], masks: Sequence[np.ndarray], cands: Dict[int, List[L.ct_schedule]],
                 cfg: W.TuneConfig, fraction: float, verify_refs: Optional[Dict[int, torch.Tensor]] = None,
-                verify_tol: float = 1e-4, pin_cores: bool = True, batch: int = 16) -> List[JobResult]:
+                verify_tol: float = 1e-4, pin_cores: bool = True, batch: int = 16,
+                log_paths: Optional[Sequence[str]] = None,
+                recorded: Optional[Dict[int, dict]] = None) -> "SharedRun":
     """Run one client per mask on a shared queue of layers, taken in the given
-    order by whichever client is idle first. Returns one JobResult per layer."""
+    order by whichever client is idle first. Returns one JobResult per layer
+    (a SharedRun, which also carries the per-client and aggregate candidates/s
+    that the library computed). log_paths: one JSON-lines log per client;
+    recorded (resume): per layer id, the candidates a log already holds."""
     keep = _Keep()
-    clients = _clients(masks, pin_cores)
+    clients = _clients(masks, pin_cores, log_paths, keep)
     jobs = (L.ct_tune_job * max(len(layers), 1))()
-    metas = [_fill_job(jobs[i], ld, cands[ld.layer_id], cfg, keep, verify_refs, verify_tol)
+    metas = [_fill_job(jobs[i], ld, cands[ld.layer_id], cfg, keep, verify_refs, verify_tol,
+                       (recorded or {}).get(ld.layer_id))
              for i, ld in enumerate(layers)]
     o1 = L.opts_from_protocol(cfg.stage1, batch=batch)
     o2 = L.opts_from_protocol(cfg.stage2, batch=cfg.top_t, interleave=1)
     owner = L.ct_tune_shared(clients, (L.ct_tune_job * len(layers)).from_address(ctypes.addressof(jobs)),
                              o1, o2, cfg.eps)
-    return [_result(jobs[i], metas[i], int(owner[i]), fraction) for i in range(len(layers))]
+    out = SharedRun(_result(jobs[i], metas[i], int(owner[i]), fraction) for i in range(len(layers)))
+    out.clients = client_stats(clients)
+    out.cands_per_s = L.ct_throughput(clients)
+    return out
+
+
+def tune_split(ld: LayerData, c: List[L.ct_schedule], cfg: W.TuneConfig, fraction: float, k: int,
+               ys: Sequence[torch.Tensor], y_ref: Optional[torch.Tensor] = None,
+               verify_tol: float = 1e-4) -> dict:
+    """One client over k CU slots (ct_tune_split): the layer's candidates are
+    screened on slots 0..k-1 of `fraction` at once, then re-measured and
+    selected on slot 0. ys: k output buffers."""
+    keep = _Keep()
+    jb = L.ct_tune_job()
+    meta = (ld,) + fill_job(jb, ld.op, ld.layer_id, ld.x, ld.w, ys[0], c, cfg.top_t, keep, y_ref, verify_tol)
+    masks = [L.ct_cu_mask(fraction, j) for j in range(k)]
+    t0 = time.perf_counter()
+    screen_s = L.ct_tune_split(jb, masks, ys[:k], L.opts_from_protocol(cfg.stage1),
+                               L.opts_from_protocol(cfg.stage2, batch=cfg.top_t, interleave=1), cfg.eps)
+    total_s = time.perf_counter() - t0
+    r = _result(jb, meta, 0, fraction)
+    return {"k": k, "screen_s": screen_s, "total_s": total_s, "screened_ok": int(np.sum(r.status1 == L.S_OK)),
+            "status_counts": {L.STATUS_NAMES[s]: int(np.sum(r.status1 == s)) for s in L.STATUS_NAMES
+                              if np.any(r.status1 == s)},
+            "winner_pos": r.winner_pos, "winner_lat_us": r.winner_lat_us, "result": r}
 
 
 def largest_first(layers: Sequence[LayerData]) -> List[LayerData]:
@@ -240,18 +313,77 @@ def tune_model_at_fraction(layers: Sequence[LayerData], cands, cfg: W.TuneConfig
     masks = [L.ct_cu_mask(fraction, j) for j in range(k)]
     if sharding == "queue":
         res = tune_shared(largest_first(layers), masks, cands, cfg, fraction, **kw)
-        return sorted(res, key=lambda r: r.layer_id)
+        res.sort(key=lambda r: r.layer_id)
+        return res
     if sharding != "round_robin":
         raise ValueError("sharding is 'queue' or 'round_robin'")
     return tune_clients(round_robin(layers, k), masks, cands, cfg, fraction, **kw)
 
 
 def fraction_report(results: Sequence[JobResult]) -> dict:
+    """Candidates, makespan and candidates/s of one share's run. For a shared
+    queue run the figures are the library's (per client and aggregate)."""
     t0 = min(r.t_start for r in results)
     t1 = max(r.t_end for r in results)
     n = sum(len(r.candidates) for r in results)
-    return {"candidates": n, "seconds": t1 - t0, "candidates_per_s": throughput(n, t0, t1),
-            "clients": len({r.client for r in results})}
+    rep = {"candidates": n, "seconds": t1 - t0, "candidates_per_s": throughput(n, t0, t1),
+           "clients": len({r.client for r in results})}
+    if isinstance(results, SharedRun):
+        rep["candidates_per_s"] = results.cands_per_s
+        rep["seconds"] = max(c.t_end for c in results.clients) - min(c.t_start for c in results.clients)
+        rep["per_client_candidates_per_s"] = [c.cands_per_s for c in results.clients]
+    return rep
+
+
+def read_logs(paths: Sequence[str]) -> dict:
+    """Merge per-client JSON-lines logs (append-only; a cut last line is
+    skipped): {"cands": {layer: {pos: (lat_us, status, family, knobs)}},
+    "jobs": {layer: record of the job's end}}. A candidate recorded twice keeps
+    its first record and is counted in "duplicates"."""
+    cands: Dict[int, dict] = {}
+    jobs: Dict[int, dict] = {}
+    dup = 0
+    for p in paths:
+        try:
+            fh = open(p)
+        except FileNotFoundError:
+            continue
+        with fh:
+            for line in fh:
+                try:
+                    rec = json.loads(line)
+                except ValueError:
+                    continue
+                if rec.get("kind") == "cand":
+                    d = cands.setdefault(int(rec["layer"]), {})
+                    pos = int(rec["pos"])
+                    if pos in d:
+                        dup += 1
+                        continue
+                    lat = rec["lat_us"]
+                    d[pos] = (float("inf") if lat is None else float(lat), int(rec["status"]), int(rec["family"]),
+                              list(rec["knobs"]))
+                elif rec.get("kind") == "job" and int(rec.get("rc", 0)) == 0:
+                    jobs[int(rec["layer"])] = rec
+    return {"cands": cands, "jobs": jobs, "duplicates": dup}
+
+
+def resume_state(logs: dict, cands: Dict[int, List[L.ct_schedule]]) -> Dict[int, dict]:
+    """Per layer id, {pos: (lat_us, status)} of recorded candidates, after
+    checking that each recorded schedule is the one at that sample position."""
+    out: Dict[int, dict] = {}
+    for layer, recs in logs["cands"].items():
+        c = cands.get(layer)
+        if c is None:
+            continue
+        d = {}
+        for pos, (lat, st, fam, knobs) in recs.items():
+            s = c[pos] if pos < len(c) else None
+            if s is None or int(s.family) != fam or [int(v) for v in s.knob[:len(knobs)]] != knobs:
+                raise ValueError("log of layer %d does not match the candidate list at position %d" % (layer, pos))
+            d[pos] = (lat, st)
+        out[layer] = d
+    return out
 
 
 def cross_eval_regret(matrices: Dict[str, list], fractions: Sequence[float]) -> List[List[float]]:

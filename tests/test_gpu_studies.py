@@ -3,9 +3,17 @@ slots (TSI scaling), latency isolation of a masked slot, and the guided
 search against the random-sample tuner."""
 import numpy as np
 import pytest
+import torch
 
 from paper_2008_03602_amd import _lib as L, studies as S, tuner as T, workloads as W
-from gpu_util import device_ready, note
+from gpu_util import device_ready, make_inputs, note, reference
+
+
+def _ref_of(ld, cfg):
+    """The oracle's output of a layer's seeded inputs, as an fp32 device tensor."""
+    x, w = make_inputs(ld.op, cfg.dist, seed=cfg.seed, config_id=cfg.config_id, layer_id=ld.layer_id)
+    ref, _ = reference(ld.op, x, w, threads=16)
+    return torch.from_numpy(ref.astype(np.float32)).to("cuda:0")
 
 pytestmark = pytest.mark.gpu
 
@@ -27,11 +35,14 @@ def test_split_screening_is_faster_and_keeps_the_winner():
     cfg = _cfg(48)
     layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops[:2])]
     cands = T.sample_all(layers, cfg)
-    note("tsi: 2 layers x k in (1, 4)")
-    rep = S.tsi_scaling(layers, cands, cfg, fraction=0.25, ks=(1, 4))
+    refs = {ld.layer_id: _ref_of(ld, cfg) for ld in layers}
+    note("tsi: 2 layers x k in (1, 4), outputs checked against the oracle")
+    rep = S.tsi_scaling(layers, cands, cfg, fraction=0.25, ks=(1, 4), verify_refs=refs)
     for row in rep["layers"]:
         for r in row["runs"]:
+            # every candidate of every slot ran, matched the oracle and was timed
             assert r["screened_ok"] == row["candidates"], row
+            assert r["status_counts"] == {"ok": row["candidates"]}, row
             assert r["winner_pos"] >= 0
         flip = row["runs"][1]
         if flip["winner_pos"] != row["runs"][0]["winner_pos"]:
@@ -53,8 +64,11 @@ def test_masked_slot_latency_holds_with_compute_neighbours():
         lat, st = L.measure_candidates_mask(op, cands, L.ct_cu_mask(0.25, 0), L.opts_from_protocol(cfg.stage1),
                                             ld.x, ld.w, ld.y)
         top = L.ct_top_t(lat, st, 4)
-        r = S.isolation(ld, [cands[i] for i in top], cfg, slots, bufs, ys)
+        r = S.isolation(ld, [cands[i] for i in top], cfg, slots, bufs, ys, y_ref=_ref_of(ld, cfg))
     print("inflation:", {k: np.round(v, 3).tolist() for k, v in r["inflation"].items()})
+    # the timed slot's outputs match the oracle whatever its neighbours run
+    for k, st in r["status"].items():
+        assert st == [L.S_OK] * len(top), (k, st)
     for k, v in r["latency_us"].items():
         assert np.all(np.isfinite(v)), k
     # four disjoint 64-CU slots running conv kernels: the masked latency moves by

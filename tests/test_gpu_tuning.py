@@ -63,26 +63,44 @@ def test_winner_repeats_or_ties_for_a_fixed_seed():
         assert gap <= 0.03, "winners differ by %.1f%%, beyond the tie band" % (100 * gap)
 
 
-def test_four_clients_run_concurrently_and_outpace_one():
-    cfg = _small_cfg(n_candidates=16, top_t=2)
-    layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops[:8])]
+def test_four_clients_run_concurrently_match_the_oracle_and_double_one():
+    # the multi-client workload: ResNet-50 b1's 22 bottleneck layers, four
+    # clients on disjoint 64-CU slots against one client on all 256 CUs, every
+    # screened candidate's output checked on the device against the oracle
+    cfg = W.config(4)
+    cfg.n_candidates = 32
+    cfg.top_t = 4
+    layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops)]
+    refs = {}
+    for ld in layers:
+        x, w = make_inputs(ld.op, cfg.dist, seed=cfg.seed, config_id=cfg.config_id, layer_id=ld.layer_id)
+        ref, _ = reference(ld.op, x, w, threads=16)
+        refs[ld.layer_id] = torch.from_numpy(ref.astype(np.float32)).to("cuda:0")
     cands = T.sample_all(layers, cfg)
-    note("4 clients x 2 layers at 25%")
-    four = T.tune_model_at_fraction(layers, cands, cfg, 0.25)
-    assert all(r.winner_pos >= 0 for r in four)
+    note("4 clients x 22 ResNet-50 layers at 25%, verified")
+    four = T.tune_model_at_fraction(layers, cands, cfg, 0.25, verify_refs=refs)
+    for r in four:
+        assert r.winner_pos >= 0
+        assert np.all(r.status1 == L.S_OK), (r.op.name, r.summary()["status_counts"])
     spans = {}
     for r in four:
         s, e = spans.get(r.client, (np.inf, -np.inf))
         spans[r.client] = (min(s, r.t_start), max(e, r.t_end))
     assert len(spans) == 4
     assert max(s for s, _ in spans.values()) < min(e for _, e in spans.values()), "clients did not overlap"
-    note("1 client x 8 layers at 100%")
+    note("1 client x 22 ResNet-50 layers at 100%, verified")
+    one = T.tune_model_at_fraction(layers, cands, cfg, 1.0, verify_refs=refs)
+    assert all(np.all(r.status1 == L.S_OK) for r in one)
+    # throughput without the verification re-runs
+    note("4 clients at 25% and 1 client at 100%, timed")
+    four = T.tune_model_at_fraction(layers, cands, cfg, 0.25)
     one = T.tune_model_at_fraction(layers, cands, cfg, 1.0)
     f4, f1 = T.fraction_report(four), T.fraction_report(one)
     ratio = f4["candidates_per_s"] / f1["candidates_per_s"]
-    print("candidates/s: 4 clients %.1f, 1 client %.1f, ratio %.2f" % (f4["candidates_per_s"],
-                                                                      f1["candidates_per_s"], ratio))
-    assert ratio > 1.3
+    print("candidates/s: 4 clients %.1f (per client %s), 1 client %.1f, ratio %.2f" % (
+        f4["candidates_per_s"], np.round(f4["per_client_candidates_per_s"], 1).tolist(), f1["candidates_per_s"],
+        ratio))
+    assert ratio >= 2.0
 
 
 def test_shared_queue_runs_every_layer_once_and_matches_round_robin_lists():
@@ -140,15 +158,16 @@ def test_cross_eval_diagonal_is_best_in_its_column():
     M = T.cross_eval(ld, winners, masks, cfg.stage2)
     print("cross-eval (us):", M.tolist())
     for j in range(len(fr)):
-        assert M[j][j] <= 1.10 * M[:, j].min(), "share %.2f: own winner %.2f us vs best %.2f us" % (
+        assert M[j][j] <= 1.03 * M[:, j].min(), "share %.2f: own winner %.2f us vs best %.2f us" % (
             fr[j], M[j][j], M[:, j].min())
 
 
 @pytest.mark.parametrize("layer", range(12))
 def test_full_size_resnet18_layers_verify_on_masked_streams(layer):
-    # every sampled candidate of the benchmark's workload, at full size, on the
-    # 25% slot-0 stream the tuner uses, checked on the device against the
-    # oracle; the last output is then compared element by element
+    # the first 12 candidates of the benchmark's 256-candidate sample of each
+    # layer (both kernel families), at full size, on the 25% slot-0 stream the
+    # tuner uses, checked on the device against the oracle; the last two
+    # outputs are then compared element by element
     cfg = W.config(2)
     op = cfg.ops[layer]
     x, w = make_inputs(op, cfg.dist, seed=cfg.seed, config_id=cfg.config_id, layer_id=layer)
