@@ -100,10 +100,12 @@ typedef struct ct_schedule {
 /* Timing protocol. Each candidate: `warmup` untimed runs, then `repeats`
  * repeats of (event record; `launches` back-to-back runs; event record).
  * Latency = median over repeats of (elapsed / launches). Candidates are
- * enqueued in groups of `batch`; the host then waits for the group's events
- * in order, polling each against a deadline: the runs enqueued before an
- * event may take at most timeout_ms each (plus 50 ms of slack for the host's
- * own scheduling), counted from when the previous event was seen complete.
+ * enqueued in groups of `batch`; the host then sleeps until a host function
+ * enqueued after the group signals that the stream has reached it. Deadlines
+ * bound the wait: the runs enqueued before an event may take at most
+ * timeout_ms each (plus 50 ms of slack for the host's own scheduling), counted
+ * from when the previous event was found complete; the events themselves are
+ * examined only when a deadline passes.
  * A candidate whose runs pass that deadline, or whose median latency exceeds
  * timeout_ms, gets CT_S_TIMEOUT. Kernels already enqueued cannot be recalled:
  * after a deadline passes the host waits for the stream to drain for

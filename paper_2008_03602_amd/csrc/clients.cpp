@@ -290,15 +290,18 @@ int ct_test_watchdog(int n_events, const int32_t* runs, const double* done_at_s,
     set_error("ct_test_watchdog: bad argument");
     return CT_E_ARG;
   }
-  double t = 0.0;  // simulated seconds; each nap advances it by 1 ms
-  int64_t naps = 0;
-  auto done = [&](int k) { return done_at_s[k] >= 0.0 && t >= done_at_s[k] ? 1 : 0; };
-  auto now = [&]() { return t; };
-  auto nap = [&]() {
-    ++naps;
-    t = (double)naps * 1e-3;
+  // simulated clock in whole milliseconds; a wait advances it 1 ms at a time
+  int64_t ms = 0;
+  auto t = [&]() { return (double)ms * 1e-3; };
+  auto done = [&](int k) { return done_at_s[k] >= 0.0 && t() >= done_at_s[k] ? 1 : 0; };
+  auto wait_until = [&](double until) {
+    for (;;) {
+      if (n_events == 0 || done(n_events - 1)) return true;
+      if (t() >= until) return false;
+      ++ms;
+    }
   };
-  const WatchResult r = watch_events(n_events, runs, run_limit_s, slack_s, drain_cap_s, done, now, nap);
+  const WatchResult r = watch_events(n_events, runs, run_limit_s, slack_s, drain_cap_s, done, wait_until, t);
   *expired_event = r.expired;
   *drained = r.drained ? 1 : 0;
   return r.rc;

@@ -143,54 +143,48 @@ int select_job(ct_tune_job* j, float eps,
                const std::function<int(const int32_t* pos, int n, float* lat2)>& remeasure);
 
 // ---- timeout watchdog ----
-// Waits for n events of one in-order stream. runs[k] kernel runs were
-// enqueued between event k-1 (or the start) and event k; each may take at most
-// run_limit_s, so event k is due run_limit_s * runs[k] + slack_s after event
-// k-1 was seen complete. done(k) reports completion (and may fail with a
-// negative code). On the first missed deadline the watchdog records the event
-// and waits up to drain_cap_s for the last event.
+// Waits for n events of one in-order stream without polling them while the
+// stream keeps pace: runs[k] kernel runs were enqueued between event k-1 (or
+// the start) and event k, each may take at most run_limit_s, so event k is due
+// run_limit_s * runs[k] + slack_s after event k-1 was found complete.
+// wait_until(t) blocks until every event has completed (returns true) or the
+// clock reaches t (returns false); only when a deadline passes is the progress
+// read, with done(k) (1 complete, 0 not, negative on failure). On the first
+// event found past its deadline the watchdog records it and waits up to
+// drain_cap_s more for the whole stream.
 struct WatchResult {
   int rc = 0;            // 0, or a negative code from done()
   int expired = -1;      // first event past its deadline, -1 if none
-  bool drained = true;   // the last event completed
+  bool drained = true;   // every event completed
 };
-template <class DoneFn, class ClockFn, class NapFn>
+template <class DoneFn, class WaitFn, class ClockFn>
 WatchResult watch_events(int n, const int32_t* runs, double run_limit_s, double slack_s,
-                         double drain_cap_s, DoneFn done, ClockFn now, NapFn nap) {
+                         double drain_cap_s, DoneFn done, WaitFn wait_until, ClockFn now) {
   WatchResult r;
   if (n <= 0) return r;
   double t_prev = now();
   int k = 0;
-  while (k < n) {
-    // in an in-order stream the last event completing means all did
-    int d = done(n - 1);
-    if (d < 0) { r.rc = d; return r; }
-    if (d) return r;
-    d = done(k);
-    if (d < 0) { r.rc = d; return r; }
-    if (d) {
-      t_prev = now();
-      ++k;
-      continue;
+  for (;;) {
+    if (k >= n) {  // every event has completed: only the completion signal is left
+      if (!wait_until(now() + drain_cap_s)) r.drained = false;
+      return r;
     }
-    if (now() > t_prev + run_limit_s * (double)runs[k] + slack_s) {
+    if (wait_until(t_prev + run_limit_s * (double)runs[k] + slack_s)) return r;
+    const int k0 = k;
+    while (k < n) {
+      const int d = done(k);
+      if (d < 0) { r.rc = d; return r; }
+      if (!d) break;
+      ++k;
+    }
+    if (k == k0) {  // no progress since the deadline of event k was set
       r.expired = k;
       break;
     }
-    nap();
+    t_prev = now();
   }
-  if (r.expired < 0) return r;
-  const double t0 = now();
-  for (;;) {
-    const int d = done(n - 1);
-    if (d < 0) { r.rc = d; return r; }
-    if (d) return r;
-    if (now() > t0 + drain_cap_s) {
-      r.drained = false;
-      return r;
-    }
-    nap();
-  }
+  if (!wait_until(now() + drain_cap_s)) r.drained = false;
+  return r;
 }
 
 }  // namespace ct

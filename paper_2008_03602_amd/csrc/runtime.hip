@@ -12,6 +12,7 @@
 #include <atomic>
 #include <chrono>
 #include <cmath>
+#include <condition_variable>
 #include <cstring>
 #include <functional>
 #include <map>
@@ -46,10 +47,19 @@ static int g_num_cus = 0;
 
 using MaskKey = std::array<uint32_t, CT_MASK_WORDS>;
 
+// Completion signal of a stream's work: a host function enqueued after the
+// work sets it (see wait_events).
+struct DrainSignal {
+  std::mutex mu;
+  std::condition_variable cv;
+  bool done = true;
+};
+
 // One CU-masked stream with everything a measurement needs on it. A context
 // is held by one call at a time (in_use) and returned to the pool after it.
 struct StreamCtx {
   MaskKey key{};
+  DrainSignal sig;
   bool in_use = false;
   bool abandoned = false;  // a wait on it was given up: never reused or synchronised
   hipStream_t stream = nullptr;
@@ -124,33 +134,87 @@ static int make_key(const uint32_t* mask, int words, MaskKey* key) {
   return CT_OK;
 }
 
+// Slot j of the partition of the device into k = num_cus / m blocks of m
+// contiguous mask bits, when the mask is one (the slots ct_build_cu_mask makes).
+static bool partition_slot(const MaskKey& key, int* m, int* j) {
+  int first = -1, last = -1, bits = 0;
+  for (int b = 0; b < g_num_cus; ++b)
+    if (key[b / 32] >> (b % 32) & 1u) {
+      if (first < 0) first = b;
+      last = b;
+      ++bits;
+    }
+  if (bits == 0 || last - first + 1 != bits || g_num_cus % bits || first % bits) return false;
+  *m = bits;
+  *j = first / bits;
+  return true;
+}
+
+static MaskKey slot_key(int m, int j) {
+  MaskKey k;
+  k.fill(0);
+  for (int b = j * m; b < (j + 1) * m; ++b) k[b / 32] |= 1u << (b % 32);
+  return k;
+}
+
+static std::mutex g_create_mu;  // stream creation, one at a time
+
 // Takes an idle context of the mask from the pool, or creates one.
+//
+// The device deals hardware queues out to its dispatch pipes in the order the
+// queues are created (measured: four CU-masked streams, one per 64-CU slot,
+// run side by side with 3-9 % latency inflation when created one after the
+// other, and with 2-3x when two of them were created four queues apart, which
+// puts them on one pipe: a kernel waiting for CUs of its own slot then holds
+// back the dispatch of the other slot's kernels). So the first use of any slot
+// of a partition into at most 8 equal contiguous slots creates the streams of
+// every slot of that partition at once, in slot order: the clients of one
+// share get consecutive queues, on distinct pipes for up to 4 slots.
 static int acquire(const MaskKey& key, Lease* lease) {
   int rc = check_init();
   if (rc) return rc;
   HIP_TRY(hipSetDevice(g_device));
-  {
+  auto take_idle = [&]() -> bool {
     std::lock_guard<std::mutex> g(g_mu);
     for (StreamCtx* c : g_pool)
       if (!c->in_use && !c->abandoned && c->key == key) {
         c->in_use = true;
         lease->set(c);
-        return CT_OK;
+        return true;
       }
+    return false;
+  };
+  if (take_idle()) return CT_OK;
+  std::lock_guard<std::mutex> cg(g_create_mu);
+  if (take_idle()) return CT_OK;  // another thread created it meanwhile
+  std::vector<MaskKey> todo;
+  int m = 0, j = 0;
+  if (partition_slot(key, &m, &j) && g_num_cus / m <= 8) {
+    std::lock_guard<std::mutex> g(g_mu);
+    for (int s = 0; s < g_num_cus / m; ++s) {
+      const MaskKey ks = slot_key(m, s);
+      bool have = false;
+      for (StreamCtx* c : g_pool) have = have || (c->key == ks && !c->abandoned);
+      if (!have || ks == key) todo.push_back(ks);
+    }
+  } else {
+    todo.push_back(key);
   }
-  StreamCtx* c = new StreamCtx();
-  c->key = key;
-  c->in_use = true;
-  hipError_t e = hipExtStreamCreateWithCUMask(&c->stream, (uint32_t)mask_words_needed(), key.data());
-  if (e != hipSuccess) {
-    delete c;
-    return hip_fail("hipExtStreamCreateWithCUMask", e);
-  }
-  {
+  StreamCtx* mine = nullptr;
+  for (const MaskKey& k : todo) {
+    StreamCtx* c = new StreamCtx();
+    c->key = k;
+    c->in_use = (k == key && !mine);
+    hipError_t e = hipExtStreamCreateWithCUMask(&c->stream, (uint32_t)mask_words_needed(), k.data());
+    if (e != hipSuccess) {
+      delete c;
+      return hip_fail("hipExtStreamCreateWithCUMask", e);
+    }
+    if (c->in_use) mine = c;
     std::lock_guard<std::mutex> g(g_mu);
     g_pool.push_back(c);
   }
-  lease->set(c);
+  lease->set(mine);
   return CT_OK;
 }
 
@@ -294,30 +358,52 @@ struct EventLog {
   }
 };
 
-// Waits for every event of the log with the watchdog. Returns CT_OK (and the
-// owner of a missed deadline in *late, -1 if none), CT_E_TIMEOUT when the
-// stream did not drain (the context is then abandoned), or CT_E_HIP.
+static void on_drain(void* p) {
+  DrainSignal* d = static_cast<DrainSignal*>(p);
+  {
+    std::lock_guard<std::mutex> g(d->mu);
+    d->done = true;
+  }
+  d->cv.notify_all();
+}
+
+// Waits for every event of the log with the watchdog. A host function enqueued
+// after the last event signals completion, so the host sleeps instead of
+// polling; an event is queried only once its deadline has passed (querying an
+// event the device has not reached makes the runtime submit extra work to
+// flush the queue, which would disturb the streams being timed). Returns CT_OK
+// (and the owner of a missed deadline in *late, -1 if none), CT_E_TIMEOUT when
+// the stream did not drain (the context is then abandoned; the signal it still
+// points to is never freed), or CT_E_HIP.
 static int wait_events(StreamCtx* c, const EventLog& lg, double run_limit_s, int* late) {
   *late = -1;
   const int n = (int)lg.ev.size();
-  int spins = 0;
+  {
+    std::lock_guard<std::mutex> g(c->sig.mu);
+    c->sig.done = false;
+  }
+  const hipError_t he = hipLaunchHostFunc(c->stream, on_drain, &c->sig);
+  if (he != hipSuccess) {
+    std::lock_guard<std::mutex> g(c->sig.mu);
+    c->sig.done = true;
+    return hip_fail("hipLaunchHostFunc", he);
+  }
   auto done = [&](int k) -> int {
     const hipError_t e = hipEventQuery(lg.ev[k]);
     if (e == hipSuccess) return 1;
     if (e == hipErrorNotReady) return 0;
     return hip_fail("hipEventQuery", e);
   };
-  auto nap = [&]() {
-    if (++spins < 4000) {
-      std::this_thread::yield();
-    } else {
-      std::this_thread::sleep_for(std::chrono::microseconds(50));
-    }
+  auto wait_until = [&](double t) -> bool {
+    using clk = std::chrono::steady_clock;
+    const auto tp = clk::time_point(std::chrono::duration_cast<clk::duration>(std::chrono::duration<double>(t)));
+    std::unique_lock<std::mutex> l(c->sig.mu);
+    return c->sig.cv.wait_until(l, tp, [&] { return c->sig.done; });
   };
   int64_t total_runs = 0;
   for (int32_t r : lg.runs) total_runs += r;
   const double drain = std::min(kDrainMaxS, std::max(kDrainMinS, 4.0 * run_limit_s * (double)total_runs));
-  const WatchResult w = watch_events(n, lg.runs.data(), run_limit_s, kSlackS, drain, done, now_s, nap);
+  const WatchResult w = watch_events(n, lg.runs.data(), run_limit_s, kSlackS, drain, done, wait_until, now_s);
   if (w.rc) return w.rc;
   if (w.expired >= 0) *late = lg.owner[w.expired];
   if (!w.drained) {

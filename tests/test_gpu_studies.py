@@ -56,7 +56,7 @@ def test_masked_slot_latency_holds_with_compute_neighbours():
     op = cfg.ops[1]
     ld = T.make_layer(op, cfg, 1)
     cands = L.ct_sample(op, cfg.seed, cfg.config_id, 1, 32)
-    note("isolation: r18.2, 4 schedules")
+    note("isolation: r18.2, 4 schedules (%d library streams)" % L.ct_stream_count())
     with S.Slots(4) as slots:
         ys = [ld.y] + [ld.y.new_empty(ld.y.shape) for _ in range(3)]
         n = 64 << 18
