@@ -25,6 +25,11 @@ library. Each function names the rule it follows.
 * A fixed GPU share per process (section 2.2) is a CU mask: m = round(n f) CUs,
   slot j = mask bits [j m, (j + 1) m).
 * Knob grids are mixed-radix numbers, first knob most significant.
+
+Pins (tests/test_oracle_host_pins.py): the published splitmix64 stream from
+state 0, shuffles and a two-family interleave worked by hand from it, and
+hand-worked quota, top-t, tie-band, mask, median and radix cases; planted
+mistakes in copies of this file are each rejected by one of them.
 """
 from __future__ import annotations
 
@@ -149,10 +154,3 @@ def select_winner(lat, pos, eps: float) -> int:
     limit = min(finite) * (1.0 + float(np.float32(eps)))
     tied = [i for i in range(len(lat)) if math.isfinite(lat[i]) and float(lat[i]) <= limit]
     return min(tied, key=lambda i: pos[i])
-
-
-def xcd_swizzle(block: int, tiles: int, xcds: int = 8) -> int:
-    """Logical tile of a block when each XCD (blocks dealt round-robin) gets a contiguous range."""
-    q, r = divmod(tiles, xcds)
-    x, idx = block % xcds, block // xcds
-    return x * (q + 1) + idx if x < r else r * (q + 1) + (x - r) * q + idx

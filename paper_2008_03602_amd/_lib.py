@@ -98,6 +98,7 @@ _SIGS = {
     "ct_tune_split": (c_i32, [P(ct_tune_job), P(c_u32), c_i32, c_i32, P(ctypes.c_void_p), P(ct_measure_opts),
                               P(ct_measure_opts), c_f32, P(c_f64)]),
     "ct_stream_count": (c_i32, []),
+    "ct_test_xcd_band": (c_i32, [c_i32, P(c_i32)]),
     "ct_test_run_clients": (c_i32, [P(ct_client), c_i32, P(ct_tune_job), c_i32, P(ct_test_hooks), P(c_i32)]),
     "ct_test_watchdog": (c_i32, [c_i32, P(c_i32), P(c_f64), c_f64, c_f64, c_f64, P(c_i32), P(c_i32)]),
     "ct_knob_values": (c_i32, [c_i32, c_i32, P(c_i32), c_i32, P(c_i32)]),
@@ -439,6 +440,13 @@ def ct_test_watchdog(runs: Sequence[int], done_at_s: Sequence[float], run_limit_
     _check(lib().ct_test_watchdog(len(r), _arr(r, c_i32), _arr(d, c_f64), run_limit_s, slack_s, drain_cap_s,
                                   ctypes.byref(ex), ctypes.byref(dr)))
     return ex.value, bool(dr.value)
+
+
+def ct_test_xcd_band(tiles: int) -> np.ndarray:
+    """Tile of each block under the bf16 family's XCD-band renumbering."""
+    out = np.zeros(tiles, dtype=np.int32)
+    _check(lib().ct_test_xcd_band(tiles, _arr(out, c_i32)))
+    return out
 
 
 def ct_cross_eval(op, scheds: Sequence, masks: Sequence, opts: ct_measure_opts, x, w, y) -> np.ndarray:

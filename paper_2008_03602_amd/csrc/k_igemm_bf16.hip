@@ -87,10 +87,7 @@ igemm_bf16_kernel(const unsigned short* __restrict__ x, const unsigned short* __
   // block -> tile (optionally renumbered so each XCD gets a contiguous range)
   const int T = a.tiles_m * a.tiles_n;
   int b = blockIdx.x;
-  if (a.swz) {
-    const int q = T / 8, r = T % 8, xcd = b % 8, idx = b / 8;
-    b = xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
-  }
+  if (a.swz) b = xcd_band_tile(b, T);
   const int tmi = b / a.tiles_n, tni = b - tmi * a.tiles_n;
   const int m0 = tmi * a.bm, n0 = tni * a.bn, sp = blockIdx.y;
 

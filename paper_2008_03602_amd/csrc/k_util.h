@@ -31,6 +31,15 @@ __device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, int off) {
 // least 1/(2d) from an integer and the fp32 product errs by less than that.
 __device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
 
+// Block renumbering for XCD locality: the device deals consecutive blocks to
+// its 8 XCDs in turn, so block b runs on XCD b mod 8. Tile of block b when
+// each XCD takes one contiguous band of the T tiles (the first T mod 8 XCDs
+// take one tile more), so neighbouring tiles share that XCD's L2.
+__host__ __device__ inline int xcd_band_tile(int b, int T) {
+  const int q = T / 8, r = T % 8, xcd = b % 8, idx = b / 8;
+  return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
 // The wave index as a scalar value, so loops bounded by per-wave values stay
 // uniform (scalar branches, unrollable) instead of exec-masked.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }

@@ -22,6 +22,7 @@
 #include <vector>
 
 #include "ct_internal.h"
+#include "k_util.h"
 
 namespace ct {
 
@@ -897,6 +898,15 @@ int ct_cross_eval(const ct_op* op, const ct_schedule* s, int n_sched, const uint
       return rc;
     for (int i = 0; i < n_sched; ++i) M[(size_t)i * n_masks + j] = st[i] == CT_S_OK ? lat[i] : INFINITY;
   }
+  return CT_OK;
+}
+
+int ct_test_xcd_band(int tiles, int32_t* tile_of_block) {
+  if (tiles < 1 || !tile_of_block) {
+    set_error("ct_test_xcd_band: bad argument");
+    return CT_E_ARG;
+  }
+  for (int b = 0; b < tiles; ++b) tile_of_block[b] = xcd_band_tile(b, tiles);
   return CT_OK;
 }
 

@@ -170,10 +170,16 @@ def test_validator_rejects_documented_cases():
         L.ct_validate(W.Op("bad", 1, 3, 4, 4, 5, 3, 3, groups=2), bad_threads)
 
 
-def test_xcd_swizzle_is_a_bijection():
+def test_bf16_block_renumbering_is_a_bijection_into_xcd_bands():
+    # the kernel's own function, through the library: every tile is taken by
+    # exactly one block, and the blocks that run on one XCD (b mod 8) take one
+    # contiguous band of tiles, in block order
     for tiles in (1, 7, 8, 9, 63, 64, 65, 196, 1000):
-        got = sorted(HR.xcd_swizzle(b, tiles) for b in range(tiles))
-        assert got == list(range(tiles))
+        got = L.ct_test_xcd_band(tiles)
+        assert sorted(got.tolist()) == list(range(tiles))
+        for x in range(8):
+            band = got[x::8].tolist()
+            assert band == list(range(band[0], band[0] + len(band))) if band else True
 
 
 def test_median_rule():
