@@ -216,6 +216,23 @@ int ct_sample(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_i
 int conv2d_run(const ct_op *op, const ct_schedule *s, const void *x, const void *w, void *y,
                const uint32_t *cu_mask, int words);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid hipMalloc): conv2d_run's work, y =
+ * conv2d(x, w) with schedule s, enqueued on the caller's HIP stream (a
+ * hipStream_t; NULL = the null stream) and returned without waiting. A
+ * schedule that splits its reduction keeps the partial sums in a static
+ * device array of CT_SCRATCH_FLOATS floats (64 MiB) that the library holds
+ * on each device until the process ends; schedules needing more than that
+ * (split * N*K*OH*OW floats) are refused with CT_E_ARG. No device memory is
+ * allocated or freed, and no stream is created. The array is shared by every
+ * call on a device and keeps the last call's contents (each split schedule
+ * overwrites every partial it reads, so nothing needs clearing): calls that
+ * overlap on one device (two streams, or two threads) race on it and must be
+ * serialised by the caller. Needs ct_init; x and w as for conv2d_run. */
+#define CT_SCRATCH_FLOATS (1 << 24)
+int conv2d_run_noalloc(const ct_op *op, const ct_schedule *s, const void *x, const void *w, void *y,
+                       void *stream);
+
 /* Time n candidates on slot 0 of the share cu_fraction, with the protocol o.
  * lat_us[i] = median latency in microseconds (+inf unless status OK),
  * status[i] = CT_S_*. rep_us (optional, n * o->repeats) receives every

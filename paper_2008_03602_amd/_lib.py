@@ -111,6 +111,8 @@ _SIGS = {
     "ct_sample": (c_i32, [P(ct_op), c_u64, c_i32, c_i32, c_i32, P(ct_schedule), P(c_i32)]),
     "conv2d_run": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                            P(c_u32), c_i32]),
+    "conv2d_run_noalloc": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_void_p]),
     "measure_candidates": (c_i32, [P(ct_op), P(ct_schedule), c_i32, c_f64, P(ct_measure_opts),
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, P(c_f32), P(c_i32)]),
     "measure_candidates_mask": (c_i32, [P(ct_op), P(ct_schedule), c_i32, P(c_u32), c_i32,
@@ -340,6 +342,17 @@ def conv2d_run(op, s: ct_schedule, x, w, y, cu_mask=None) -> None:
     m = mask_array(cu_mask) if cu_mask is not None else None
     _check(lib().conv2d_run(ctypes.byref(o), ctypes.byref(s), _ptr(x), _ptr(w), _ptr(y), m,
                             MASK_WORDS if m is not None else 0))
+
+
+SCRATCH_FLOATS = 1 << 24
+
+
+def conv2d_run_noalloc(op, s: ct_schedule, x, w, y, stream: int = 0) -> None:
+    """conv2d_run without any allocation: enqueued on `stream` (a raw HIP
+    stream handle, 0 = the null stream), returns without waiting."""
+    o = make_op(op)
+    _check(lib().conv2d_run_noalloc(ctypes.byref(o), ctypes.byref(s), _ptr(x), _ptr(w), _ptr(y),
+                                    ctypes.c_void_p(stream) if stream else None))
 
 
 def measure_candidates(op, scheds: Sequence, cu_fraction: float, opts: ct_measure_opts, x, w, y):

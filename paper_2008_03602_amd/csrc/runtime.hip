@@ -46,6 +46,15 @@ static std::mutex g_mu;  // guards the device state, the stream pool and the ref
 static int g_device = -1;
 static int g_num_cus = 0;
 
+// Split partial sums of conv2d_run_noalloc: a static array in device memory,
+// one copy on every device the library runs on, held until the process ends.
+// Host code never uses its name as an address: ct_init looks up the device
+// address of the initialised device's copy (g_scratch_dev) and the launches
+// take that.
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) float scratch[CT_SCRATCH_FLOATS];
+static float* g_scratch_dev[kMaxDevices] = {};
+
 using MaskKey = std::array<uint32_t, CT_MASK_WORDS>;
 
 // Completion signal of a stream's work: a host function enqueued after the
@@ -657,6 +666,15 @@ int ct_init(int device) {
     set_error("ct_init: unexpected CU count");
     return CT_E_NODEV;
   }
+  if (device >= kMaxDevices) {
+    set_error("ct_init: device index beyond the library's table");
+    return CT_E_ARG;
+  }
+  if (!g_scratch_dev[device]) {  // this device's copy of the static scratch array
+    float* ptr = nullptr;
+    HIP_TRY(hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)));
+    g_scratch_dev[device] = ptr;
+  }
   g_num_cus = p.multiProcessorCount;
   g_device = device;
   return CT_OK;
@@ -747,6 +765,38 @@ int conv2d_run(const ct_op* op, const ct_schedule* s, const void* x, const void*
   if (lrc == -2) return CT_E_ARG;  // the launcher refused the arguments (reason already set)
   if (lrc != 0) return hip_fail("conv2d_run launch", hipGetLastError());
   HIP_TRY(hipStreamSynchronize(c->stream));
+  return CT_OK;
+}
+
+int conv2d_run_noalloc(const ct_op* op, const ct_schedule* s, const void* x, const void* w, void* y,
+                       void* stream) {
+  OpX ox;
+  int rc = derive_checked(op, &ox);
+  if (rc) return rc;
+  if (!s || !x || !w || !y) {
+    set_error("conv2d_run_noalloc: null argument");
+    return CT_E_ARG;
+  }
+  if ((rc = check_init())) return rc;
+  Geom g;
+  std::string why;
+  if (compute_geom(ox, *s, &g, &why) != CT_OK) {
+    set_error("conv2d_run_noalloc: invalid schedule: " + why);
+    return CT_E_ARG;
+  }
+  if (g.ws_floats > (int64_t)CT_SCRATCH_FLOATS) {
+    set_error("conv2d_run_noalloc: the schedule's split partial sums need " + std::to_string(g.ws_floats) +
+              " floats; the static scratch array holds " + std::to_string((int64_t)CT_SCRATCH_FLOATS));
+    return CT_E_ARG;
+  }
+  float* ws = g_scratch_dev[g_device];
+  if (!ws) {
+    set_error("conv2d_run_noalloc: no scratch address for the device");
+    return CT_E_NOINIT;
+  }
+  const int lrc = launch_once(ox, *s, g, x, w, y, ws, (hipStream_t)stream);
+  if (lrc == -2) return CT_E_ARG;  // the launcher refused the arguments (reason already set)
+  if (lrc != 0) return hip_fail("conv2d_run_noalloc launch", hipGetLastError());
   return CT_OK;
 }
 
