@@ -54,7 +54,7 @@ bool family_applies(int family, const OpX& x);
 // ---- per-family geometry ----
 // Knob positions of each family, in table order.
 namespace direct_knob { enum { TOH, TOW, TK, MK, MW, LDS, CT, SPLIT, UNR, COUNT }; }
-namespace dw_knob { enum { TC, TOH, TOW, VEC, RPT, LDS, NB, ORDER, COUNT }; }
+namespace dw_knob { enum { TC, TOH, TOW, VEC, RPT, LDS, NB, ORDER, Q4, COUNT }; }
 namespace bf16_knob { enum { MF, TM, TN, WM, WN, KC, LDS, SPLIT, SWZ, COUNT }; }
 namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, TPW, CPC, STAGES, SPLIT, COUNT }; }
 

@@ -9,6 +9,11 @@
 // LDS = 1 stages the input halo tile of the block once; LDS = 0 reads taps
 // straight from global memory (L1/L2 absorb the overlap). ORDER picks the
 // block numbering: tiles fastest (0) or channel groups fastest (1).
+// Q4 = 1 (3x3 filters with pad 1 only) switches to depthwise_q4_kernel: a
+// thread owns 4 consecutive output columns of RPT consecutive rows, reads
+// each input row it needs once with 16-byte loads (plus the edge words) and
+// keeps the taps in registers, so a wave reads and writes whole 16-byte
+// words and an output costs well under one load instruction instead of nine.
 // Every global access is bounds-checked.
 #include <hip/hip_runtime.h>
 
@@ -24,6 +29,7 @@ struct DwArgs {
   int tiles_h, tiles_w, tiles_c, tiles_n;
   int ih_t, iw_t;
   int threads, rows, cols;
+  int vec_ld, vec_st;  // depthwise_q4_kernel: 16-byte input loads / output stores allowed
 };
 
 __host__ __device__ constexpr int dw_spec_r(int spec) { return spec == 3 || spec == 4 ? 3 : 0; }
@@ -151,7 +157,117 @@ depthwise_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, f
   }
 }
 
+typedef float dwf4 __attribute__((ext_vector_type(4)));
+
+// 3x3, pad 1, stride STRIDE: a thread computes 4 consecutive output columns of
+// RPT consecutive output rows of one (image, channel) plane. It reads the
+// (RPT - 1) * STRIDE + 3 input rows those outputs need, each as the
+// 3 * STRIDE + 3 columns from ow * STRIDE - 1 on: with vec_ld, the interior
+// 4 (stride 1) or 8 (stride 2) columns as 16-byte loads and the edge columns
+// as words (which the neighbouring lanes' 16-byte loads have brought into
+// L1). vec_ld holds when W is a multiple of 4, W = STRIDE * OW, OW is a
+// multiple of 4 and x is 16-byte aligned: every 16-byte load then lies inside
+// its row. Columns and rows outside the image read as zero.
+template <int STRIDE, int RPT>
+__global__ void __launch_bounds__(1024)
+depthwise_q4_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ y, DwArgs a) {
+  constexpr int NIN = (RPT - 1) * STRIDE + 3;  // input rows read
+  constexpr int NCOL = 3 * STRIDE + 3;         // input columns per row
+  const int H = a.H, W = a.W, C = a.C, OH = a.OH, OW = a.OW;
+
+  int b = blockIdx.x, tw, th, cg, ng;
+  if (a.order == 0) {
+    tw = b % a.tiles_w; b /= a.tiles_w;
+    th = b % a.tiles_h; b /= a.tiles_h;
+    cg = b % a.tiles_c; ng = b / a.tiles_c;
+  } else {
+    cg = b % a.tiles_c; b /= a.tiles_c;
+    tw = b % a.tiles_w; b /= a.tiles_w;
+    th = b % a.tiles_h; ng = b / a.tiles_h;
+  }
+  int t = threadIdx.x;
+  const int colq = t % a.cols; t /= a.cols;
+  const int rowg = t % a.rows; t /= a.rows;
+  const int ci = t % a.tc;
+  const int ni = t / a.tc;
+  const int c = cg * a.tc + ci, n = ng * a.nb + ni;
+  const int ow = tw * a.tow + 4 * colq, oh = th * a.toh + rowg * RPT;
+  if (c >= C || n >= a.N || ow >= OW || oh >= OH) return;  // no barriers in this kernel
+
+  float wv[9];
+#pragma unroll
+  for (int i = 0; i < 9; ++i) wv[i] = w[(int64_t)c * 9 + i];
+  const float* xp = x + ((int64_t)n * C + c) * H * W;
+  const int ih0 = oh * STRIDE - 1, iw0 = ow * STRIDE - 1;
+
+  float acc[RPT][4];
+#pragma unroll
+  for (int u = 0; u < RPT; ++u)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[u][j] = 0.f;
+
+#pragma unroll
+  for (int i = 0; i < NIN; ++i) {
+    const int ih = ih0 + i;
+    float v[NCOL];
+#pragma unroll
+    for (int k = 0; k < NCOL; ++k) v[k] = 0.f;
+    if ((unsigned)ih < (unsigned)H) {
+      const float* row = xp + (int64_t)ih * W;
+      if (a.vec_ld) {
+        v[0] = iw0 >= 0 ? row[iw0] : 0.f;
+        const dwf4 q0 = *(const dwf4*)(row + iw0 + 1);
+        v[1] = q0.x; v[2] = q0.y; v[3] = q0.z; v[4] = q0.w;
+        if constexpr (STRIDE == 1) {
+          v[5] = iw0 + 5 < W ? row[iw0 + 5] : 0.f;
+        } else {
+          const dwf4 q1 = *(const dwf4*)(row + iw0 + 5);
+          v[5] = q1.x; v[6] = q1.y; v[7] = q1.z; v[8] = q1.w;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < NCOL; ++k) v[k] = load_or_zero(row, iw0 + k, (unsigned)(iw0 + k) < (unsigned)W);
+      }
+    }
+    // input row i feeds output row u through filter row r = i - u * STRIDE
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
+      const int r = i - u * STRIDE;
+      if (r < 0 || r > 2) continue;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int s = 0; s < 3; ++s) acc[u][j] = fmaf(wv[r * 3 + s], v[j * STRIDE + s], acc[u][j]);
+    }
+  }
+
+  float* yp = y + ((int64_t)n * C + c) * OH * OW;
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) {
+    if (oh + u >= OH) break;
+    float* o = yp + (int64_t)(oh + u) * OW + ow;
+    if (a.vec_st) {
+      dwf4 q;
+      q.x = acc[u][0]; q.y = acc[u][1]; q.z = acc[u][2]; q.w = acc[u][3];
+      *(dwf4*)o = q;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (ow + j < OW) o[j] = acc[u][j];
+    }
+  }
+}
+
 using DwFn = void (*)(const float*, const float*, float*, DwArgs);
+
+template <int STRIDE>
+static DwFn dw_q4_pick(int rpt) {
+  switch (rpt) {
+    case 1: return depthwise_q4_kernel<STRIDE, 1>;
+    case 2: return depthwise_q4_kernel<STRIDE, 2>;
+    default: return depthwise_q4_kernel<STRIDE, 4>;
+  }
+}
 
 template <int VEC, int RPT, bool LDS>
 static DwFn dw_pick_spec(int spec) {
@@ -196,7 +312,17 @@ int launch_depthwise_f32(const OpX& x, const ct_schedule& s, const Geom& g, cons
   a.rows = a.toh / s.knob[RPT];
   a.cols = a.tow / s.knob[VEC];
   // the 3x3 specialisation needs pad 1 and dilation 1, which op_spec checks
-  DwFn fn = dw_pick(s.knob[VEC], s.knob[RPT], s.knob[LDS], g.spec);
+  DwFn fn;
+  if (s.knob[Q4]) {  // the validator admits it for 3x3 pad-1 ops (spec 3 or 4) with VEC = 4, LDS = 0
+    const int st = g.spec == SPEC_3X3_S2 ? 2 : 1;
+    a.cols = a.tow / 4;
+    a.vec_ld = a.W % 4 == 0 && a.W == st * a.OW && a.OW % 4 == 0 && ((uintptr_t)xin % 16) == 0;
+    a.vec_st = a.OW % 4 == 0 && ((uintptr_t)y % 16) == 0;
+    fn = st == 2 ? dw_q4_pick<2>(s.knob[RPT]) : dw_q4_pick<1>(s.knob[RPT]);
+  } else {
+    a.vec_ld = a.vec_st = 0;
+    fn = dw_pick(s.knob[VEC], s.knob[RPT], s.knob[LDS], g.spec);
+  }
   hipLaunchKernelGGL(fn, dim3((unsigned)g.blocks), dim3(g.threads), g.lds_bytes, (hipStream_t)stream,
                      (const float*)xin, (const float*)w, (float*)y, a);
   return hipGetLastError() == hipSuccess ? 0 : -1;

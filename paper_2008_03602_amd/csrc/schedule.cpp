@@ -35,7 +35,8 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"rpt", 3, {1, 2, 4}},
       {"lds", 2, {0, 1}},
       {"nb", 3, {1, 2, 4}},
-      {"order", 2, {0, 1}}}},
+      {"order", 2, {0, 1}},
+      {"q4", 2, {0, 1}}}},
     {CT_FAM_IGEMM_BF16, "igemm_mfma_bf16", bf16_knob::COUNT,
      {{"mfma", 2, {16, 32}},
       {"tm", 3, {1, 2, 4}},
@@ -226,6 +227,12 @@ static int geom_depthwise(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const ct_op& o = x.op;
   const int tc = s.knob[TC], toh = s.knob[TOH], tow = s.knob[TOW], vec = s.knob[VEC];
   const int rpt = s.knob[RPT], lds = s.knob[LDS], nb = s.knob[NB];
+  if (s.knob[Q4]) {
+    // 4 consecutive output columns per thread, registers only, 3x3 pad 1
+    if (g->spec != SPEC_3X3_S1 && g->spec != SPEC_3X3_S2) REJECT("q4 needs a 3x3 filter with pad 1");
+    if (vec != 4) REJECT("q4 takes 4 output columns per thread (vec 4)");
+    if (lds) REJECT("q4 reads rows into registers (lds 0)");
+  }
   if (tow % vec) REJECT("tow not a multiple of vec");
   if (toh % rpt) REJECT("toh not a multiple of rpt");
   if (toh > fit(f.knobs[TOH], x.oh)) REJECT("toh exceeds the output height");
@@ -555,8 +562,11 @@ int ct_kernel_name(const ct_op* op, const ct_schedule* s, char* buf, int cap) {
       break;
     case CT_FAM_DEPTHWISE_F32: {
       const int spec = g.spec == SPEC_3X3_S1 ? 3 : (g.spec == SPEC_3X3_S2 ? 4 : 0);
-      std::snprintf(tmp, sizeof tmp, "depthwise_f32_kernel<%d, %d, %s, %d>", k[dw_knob::VEC], k[dw_knob::RPT],
-                    tf(k[dw_knob::LDS]), spec);
+      if (k[dw_knob::Q4])
+        std::snprintf(tmp, sizeof tmp, "depthwise_q4_kernel<%d, %d>", spec == SPEC_3X3_S2 ? 2 : 1, k[dw_knob::RPT]);
+      else
+        std::snprintf(tmp, sizeof tmp, "depthwise_f32_kernel<%d, %d, %s, %d>", k[dw_knob::VEC], k[dw_knob::RPT],
+                      tf(k[dw_knob::LDS]), spec);
       break;
     }
     case CT_FAM_IGEMM_BF16:

@@ -97,7 +97,7 @@ class JobResult:
 def describe_schedule(op: W.Op, s: L.ct_schedule) -> dict:
     nk, _ = L.ct_grid_info(s.family)
     names = {1: ["toh", "tow", "tk", "mk", "mw", "lds", "ct", "split", "unroll"],
-             2: ["tc", "toh", "tow", "vec", "rpt", "lds", "nb", "order"],
+             2: ["tc", "toh", "tow", "vec", "rpt", "lds", "nb", "order", "q4"],
              3: ["mfma", "tm", "tn", "wm", "wn", "kc", "lds", "split", "swizzle"],
              4: ["mfma", "tm", "tn", "wm", "wn", "ws", "tpw", "cpc", "stages", "split"]}[s.family]
     d = {"family": W.FAMILY_NAMES[s.family], "knobs": {names[i]: int(s.knob[i]) for i in range(nk)},

@@ -117,6 +117,43 @@ def test_depthwise_matches_oracle(op):
     _run_sample(op, 24, seed=12)
 
 
+# 3x3 pad-1 depthwise shapes for the 4-columns-per-thread variant: 16-byte
+# loads and stores (W a multiple of 4, W = stride * OW, OW a multiple of 4),
+# and the word-by-word fallback (odd widths, W != 2 OW), with ragged tiles
+Q4_OPS = [
+    W.conv("dwq_s1", 2, 12, 20, 12, 3, 1, 1, groups=12),
+    W.conv("dwq_s2", 3, 8, 24, 8, 3, 2, 1, groups=8),
+    W.conv("dwq_odd", 2, 13, 15, 13, 3, 1, 1, groups=13),
+    W.conv("dwq_s2odd", 1, 6, 17, 6, 3, 2, 1, groups=6),
+    W.conv("dwq_s2w14", 2, 10, 14, 10, 3, 2, 1, groups=10),
+]
+
+
+def _q4_sample(op, n, seed):
+    space = [s for s in L.ct_valid_space(op) if s.family == W.FAM_DEPTHWISE_F32 and s.knob[8] == 1]
+    assert space, op.name
+    return random.Random(seed).sample(space, min(n, len(space)))
+
+
+@pytest.mark.parametrize("op", Q4_OPS, ids=lambda o: o.name)
+def test_depthwise_q4_matches_oracle_and_is_exact_on_integers(op):
+    x, w = make_inputs(op, "uniform", seed=31)
+    ref, a = reference(op, x, w)
+    xi, wi = make_inputs(op, "int", seed=32)
+    refi, _ = reference(op, xi, wi)
+    xd, wd, yd = to_device(op, x, w)
+    xid, wid, yid = to_device(op, xi, wi)
+    for s in _q4_sample(op, 16, seed=33):
+        tag = "%s %s" % (op.name, sched_str(s))
+        note(tag)
+        yd.fill_(float("nan"))
+        L.conv2d_run(op, s, xd, wd, yd)
+        check_close(op, yd.cpu().numpy(), ref, a, tag)
+        yid.fill_(float("nan"))
+        L.conv2d_run(op, s, xid, wid, yid)
+        assert np.array_equal(yid.cpu().numpy().astype(np.float64), refi), tag + ": not bit-exact on integers"
+
+
 @pytest.mark.parametrize("op", BF_OPS, ids=lambda o: o.name)
 def test_bf16_pointwise_matches_oracle(op):
     _run_sample(op, 24, seed=13)
