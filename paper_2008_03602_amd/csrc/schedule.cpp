@@ -195,7 +195,10 @@ static int geom_direct(const OpX& x, const ct_schedule& s, Geom* g, std::string*
   if (4 * x.nx >= ((int64_t)1 << 31) || 4 * x.nw >= ((int64_t)1 << 31))
     REJECT("tensor too large for 32-bit buffer offsets");
   const int64_t threads = (int64_t)(tk / mk) * (toh * tow / mw);
-  if (threads < kMinThreads || threads > kMaxThreads) REJECT("threads per block out of range");
+  // fewer threads than half a wave only where the tile already spans the whole
+  // op (an op smaller than a wave): the block's other lanes stay masked off
+  const bool spans = toh >= x.oh && tow >= x.ow && tk >= o.k;
+  if ((threads < kMinThreads && !spans) || threads > kMaxThreads) REJECT("threads per block out of range");
   // the register budget of the kernel's launch bounds: an accumulator tile of
   // 16 or more outputs per thread allows at most 512 threads
   if (mk * mw >= 16 && threads > 512) REJECT("too many threads for the accumulator tile");
@@ -240,7 +243,8 @@ static int geom_depthwise(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   if (tc > fit(f.knobs[TC], o.c)) REJECT("tc exceeds C");
   if (nb > fit(f.knobs[NB], o.n)) REJECT("nb exceeds N");
   const int64_t threads = (int64_t)tc * nb * (toh / rpt) * (tow / vec);
-  if (threads < kMinThreads || threads > kMaxThreads) REJECT("threads per block out of range");
+  const bool spans = tc >= o.c && nb >= o.n && toh >= x.oh && tow >= x.ow;  // as for the direct family
+  if ((threads < kMinThreads && !spans) || threads > kMaxThreads) REJECT("threads per block out of range");
   g->ih_t = (int)((toh - 1) * o.stride_h + (o.r - 1) * o.dil_h + 1);
   g->iw_t = (int)((tow - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1);
   int64_t lbytes = lds ? 4 * (int64_t)tc * nb * g->ih_t * g->iw_t : 0;
