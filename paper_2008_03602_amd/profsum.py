@@ -39,6 +39,8 @@ CSRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
 
 # kernel name prefix -> the source files that define it
 PEAK_FP32_TFLOPS = 157.3  # MI355X dense fp32 (vector and MFMA), 256 CUs at 2.4 GHz
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA
+PEAK_HBM_TBPS = 8.0        # MI355X HBM3E
 
 _KERNEL_SOURCES = {
     "direct_f32_kernel": ["k_direct*"],
@@ -62,6 +64,14 @@ def kernel_source_hash(kernel: str) -> str | None:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def _lds_ok(traced, requested) -> bool:
+    """A trace may list a dispatch's LDS as allocated, rounded up to the
+    allocation granule: accept up to 1 KiB above the bytes the launch asked for."""
+    if requested is None:
+        return True
+    return traced is not None and requested <= traced <= requested + 1024
 
 
 def short_name(name: str) -> str:
@@ -98,7 +108,7 @@ class Trace:
              "stream_id, duration FROM kernels WHERE name LIKE ?")
         for n, w, g, l, st, d in self.db.execute(q, ("%" + kernel + "%",)):
             if (kernel in n.replace("void ", "") and (wg is None or w == wg) and (grid is None or g == grid)
-                    and (lds is None or l == lds)):
+                    and _lds_ok(l, lds)):
                 out[st].append(d)
         return out
 
@@ -129,7 +139,7 @@ class Trace:
             rows = [(n, w, g, l, d) for n, g, w, l, d in self.rows if kernel in n]
         return [d for n, w, g, l, d in rows
                 if kernel in n.replace("void ", "") and (wg is None or w == wg) and (grid is None or g == grid)
-                and (lds is None or l == lds)]
+                and _lds_ok(l, lds)]
 
 
 def _int(r, *names):
@@ -260,6 +270,16 @@ def summarize(trace_dir, bench=None, replay=None, fetch_dir=None, write_dir=None
                              len(rdurs), tavg, statistics.median(rdurs) / 1e3, ttf,
                              100 * ttf / (PEAK_FP32_TFLOPS * replay["fraction"]), PEAK_FP32_TFLOPS,
                              replay["fraction"]))
+            if replay.get("bytes_moved"):
+                # |x| + |w| + |y| once per launch: the bound of the memory-bound families
+                tbps = replay["bytes_moved"] / (tavg * 1e-6) / 1e12
+                lines.append("Algorithmic bytes (|x| + |w| + |y|) %d per launch: from the trace average %.2f TB/s "
+                             "= %.1f%% of the %.1f TB/s HBM peak (which does not scale with the CU share)." % (
+                                 replay["bytes_moved"], tbps, 100 * tbps / PEAK_HBM_TBPS, PEAK_HBM_TBPS))
+                if replay.get("dtype") == "bf16":
+                    lines.append("The bf16 MFMA side: %.2f TFLOP/s = %.2f%% of %.1f TFLOP/s x %g." % (
+                        ttf, 100 * ttf / (PEAK_BF16_TFLOPS * replay["fraction"]), PEAK_BF16_TFLOPS,
+                        replay["fraction"]))
             if sh.get("kernels", 1) > 1:
                 red = tr.durations("split_reduce_kernel", None, None)
                 if red:

@@ -443,7 +443,9 @@ def replay(layer: str, family: int, knobs: Sequence[int], fraction: float, launc
     lat, st = L.measure_candidates_mask(op, [s], mask, L.make_opts(1, 1, launches, 1), ld.x, ld.w, ld.y)
     out = {"layer": layer, "kernel": L.ct_kernel_name(op, s), "schedule": describe_schedule(op, s),
            "fraction": fraction, "launches": launches, "status": int(st[0]), "latency_us": float(lat[0]),
-           "tflops": op.flops() / (float(lat[0]) * 1e-6) / 1e12}
+           "tflops": op.flops() / (float(lat[0]) * 1e-6) / 1e12, "flops": op.flops(),
+           "bytes_moved": op.bytes_moved(), "tbps": op.bytes_moved() / (float(lat[0]) * 1e-6) / 1e12,
+           "dtype": "bf16" if op.dtype == W.DT_BF16 else "f32"}
     if copy_mib > 0:
         n = copy_mib * (1 << 20)
         src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
