@@ -107,6 +107,9 @@ def main() -> int:
     ap.add_argument("--budget-s", type=float, default=420.0,
                     help="stop starting steps once the run has used this many seconds")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--uniform", action="store_true",
+                    help="sample each layer's 256 candidates uniformly from its whole valid space "
+                         "(no equal shares per kernel family)")
     ap.add_argument("--report", default=None, help="write the per-step, per-layer report (JSON) here")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -122,7 +125,7 @@ def main() -> int:
     L.ct_init(0)
     cfg = W.config(2)
     layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops)]
-    full = T.sample_all(layers, cfg)
+    full = T.sample_all(layers, cfg, uniform=a.uniform)
     n_batches = max(1, (cfg.n_candidates + SLICE - 1) // SLICE)
     masks = [L.ct_cu_mask(f, 0) for f in FRACTIONS]
 
@@ -233,10 +236,12 @@ def main() -> int:
         "ms_per_step": elapsed / n_steps * 1e3, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": "ResNet-18 b1 conv set (12 layers) fp32 NCHW, 256 seeded candidates per layer "
-                               "(equal shares per kernel family) in 8 fixed batches of 32; one step = one batch of "
+                               "(%s) in 8 fixed batches of 32; one step = one batch of "
                                "every layer tuned at 25/50/100%% CUs by 4/2/1 concurrent CU-masked clients sharing "
                                "a largest-first layer queue (screen, top-%d re-measure, tie rule), then a 3x3 "
-                               "cross-evaluation of the winners" % cfg.top_t,
+                               "cross-evaluation of the winners"
+                               % ("uniform over the valid space" if a.uniform else "equal shares per kernel family",
+                                  cfg.top_t),
                    "candidates_per_step": steps[0]["screened"], "layers": len(layers), "seed": cfg.seed,
                    "batches_timed": sorted({st["batch"] for st in steps}),
                    "steps_requested": a.steps,

@@ -206,6 +206,15 @@ int ct_valid_space(const ct_op *op, ct_schedule *out, int64_t cap, int64_t *coun
 int ct_sample(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_id,
               int32_t n, ct_schedule *out, int32_t *n_out);
 
+/* The same without family quotas: the first n positions of one seeded partial
+ * Fisher-Yates shuffle of the whole valid space (ct_valid_space order),
+ * splitmix64 from state seed ^ (0x9E3779B97F4A7C15 * (1 + config_id)) ^
+ * (0xC0FFEE << 32) ^ layer_id, first output discarded; j = i + next() mod
+ * (|V| - i). Every valid schedule is equally likely, so a family's share of
+ * the sample follows the size of its knob grid. */
+int ct_sample_uniform(const ct_op *op, uint64_t seed, int32_t config_id, int32_t layer_id,
+                      int32_t n, ct_schedule *out, int32_t *n_out);
+
 /* ---- running and timing (section 2.1 stage 3, "profile") ---- */
 
 /* Run schedule s once on op: y = conv2d(x, w). cu_mask = NULL uses all CUs.

@@ -72,6 +72,14 @@ def partial_shuffle(size: int, take: int, state: int) -> List[int]:
     return out
 
 
+def uniform_positions(size: int, n: int, seed: int, config_id: int, layer_id: int) -> List[int]:
+    """The sample without family quotas: the first n positions of one partial
+    shuffle of the whole valid list, from the state without the family term."""
+    state = (seed ^ ((GAMMA * (1 + config_id)) & MASK64) ^ ((0xC0FFEE << 32) & MASK64)
+             ^ (layer_id & 0xFFFFFFFF)) & MASK64
+    return partial_shuffle(size, n, state)
+
+
 def family_quotas(sizes: Sequence[int], n: int) -> List[int]:
     """Equal shares of min(n, total), the remainder to the first families; a
     family smaller than its share hands the rest on, round after round."""

@@ -109,6 +109,7 @@ _SIGS = {
     "ct_kernel_name": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_char_p, c_i32]),
     "ct_valid_space": (c_i32, [P(ct_op), P(ct_schedule), c_i64, P(c_i64)]),
     "ct_sample": (c_i32, [P(ct_op), c_u64, c_i32, c_i32, c_i32, P(ct_schedule), P(c_i32)]),
+    "ct_sample_uniform": (c_i32, [P(ct_op), c_u64, c_i32, c_i32, c_i32, P(ct_schedule), P(c_i32)]),
     "conv2d_run": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                            P(c_u32), c_i32]),
     "conv2d_run_noalloc": (c_i32, [P(ct_op), P(ct_schedule), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -334,6 +335,14 @@ def ct_sample(op, seed: int, config_id: int, layer_id: int, n: int) -> List[ct_s
     arr = (ct_schedule * max(n, 1))()
     got = c_i32()
     _check(lib().ct_sample(ctypes.byref(o), seed, config_id, layer_id, n, arr, ctypes.byref(got)))
+    return [arr[i] for i in range(got.value)]
+
+
+def ct_sample_uniform(op, seed: int, config_id: int, layer_id: int, n: int) -> List[ct_schedule]:
+    o = make_op(op)
+    arr = (ct_schedule * max(n, 1))()
+    got = c_i32()
+    _check(lib().ct_sample_uniform(ctypes.byref(o), seed, config_id, layer_id, n, arr, ctypes.byref(got)))
     return [arr[i] for i in range(got.value)]
 
 

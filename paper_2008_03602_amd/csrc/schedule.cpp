@@ -688,6 +688,25 @@ int ct_sample(const ct_op* op, uint64_t seed, int32_t config_id, int32_t layer_i
   return CT_OK;
 }
 
+int ct_sample_uniform(const ct_op* op, uint64_t seed, int32_t config_id, int32_t layer_id, int32_t n,
+                      ct_schedule* out, int32_t* n_out) {
+  if (!op || !out || !n_out || n < 0) { set_error("ct_sample_uniform: bad argument"); return CT_E_ARG; }
+  std::vector<ct_schedule> v;
+  int rc = valid_space(op, &v);
+  if (rc) return rc;
+  uint64_t state = seed ^ (0x9E3779B97F4A7C15ull * (uint64_t)(1 + (int64_t)config_id)) ^ (0xC0FFEEull << 32) ^
+                   (uint64_t)(uint32_t)layer_id;
+  splitmix64_next(&state);  // the first output is discarded
+  const uint64_t size = v.size(), take = std::min<uint64_t>((uint64_t)n, size);
+  for (uint64_t i = 0; i < take; ++i) {
+    const uint64_t j = i + splitmix64_next(&state) % (size - i);
+    std::swap(v[i], v[j]);
+    out[i] = v[i];
+  }
+  *n_out = (int32_t)take;
+  return CT_OK;
+}
+
 int ct_top_t(const float* lat_us, const int32_t* status, int n, int t, int32_t* top, int32_t* n_top) {
   if (!lat_us || !status || !top || !n_top || n < 0 || t < 0) { set_error("ct_top_t: bad argument"); return CT_E_ARG; }
   std::vector<int32_t> ok;

@@ -31,6 +31,14 @@ PEAK_FP32_TFLOPS = 157.3      # MI355X vector / matrix fp32, 256 CUs at 2.4 GHz
 PEAK_BF16_TFLOPS = 2516.6     # dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0
 
+# Concurrent clients per CU share. The device deals hardware queues to 4
+# dispatch pipes in creation order, and the library creates a share's slot
+# streams one after another, so slots j and j + 4 of a share land on one pipe.
+# Measured at 12.5 % (8 slots of 32 CUs): the one neighbour on slot 0's pipe
+# inflates slot 0's latencies 1.8-2.5x, the six on other pipes 1.06-1.10x
+# together. So a share runs at most 4 clients (one per pipe), on slots 0-3.
+MAX_CLIENTS = 4
+
 
 @dataclass
 class LayerData:
@@ -296,9 +304,11 @@ def throughput(n_candidates: int, t_first_start: float, t_last_end: float) -> fl
     return n_candidates / span if span > 0 else float("nan")
 
 
-def sample_all(layers: Sequence[LayerData], cfg: W.TuneConfig) -> Dict[int, List[L.ct_schedule]]:
-    return {ld.layer_id: L.ct_sample(ld.op, cfg.seed, cfg.config_id, ld.layer_id, cfg.n_candidates)
-            for ld in layers}
+def sample_all(layers: Sequence[LayerData], cfg: W.TuneConfig, uniform: bool = False) -> Dict[int, List[L.ct_schedule]]:
+    """Each layer's seeded candidate list: equal shares per kernel family
+    (ct_sample), or one shuffle of the whole valid space (ct_sample_uniform)."""
+    f = L.ct_sample_uniform if uniform else L.ct_sample
+    return {ld.layer_id: f(ld.op, cfg.seed, cfg.config_id, ld.layer_id, cfg.n_candidates) for ld in layers}
 
 
 def tune_model_at_fraction(layers: Sequence[LayerData], cands, cfg: W.TuneConfig, fraction: float,
@@ -308,7 +318,7 @@ def tune_model_at_fraction(layers: Sequence[LayerData], cands, cfg: W.TuneConfig
 
     sharding "queue": the clients take layers from one queue, largest first;
     "round_robin": layer i goes to client i mod k, in table order."""
-    k = clients or max(1, int(round(1.0 / fraction)))
+    k = clients or min(MAX_CLIENTS, max(1, int(round(1.0 / fraction))))
     k = min(k, len(layers))
     masks = [L.ct_cu_mask(fraction, j) for j in range(k)]
     if sharding == "queue":
@@ -418,6 +428,31 @@ def model_aggregates(matrices: Dict[str, list], fractions: Sequence[float]) -> d
             "mean_ratio_per_tuning_share": mean.tolist(), "sweet_spot": float(fractions[int(np.argmin(mean))])}
 
 
+def determinism_report(runs: Sequence[dict], layers: Sequence[LayerData], cands, cfg: W.TuneConfig) -> dict:
+    """Winners of repeated tunings with one seed: the candidate lists are
+    identical by construction; a winner may differ only inside the tie band.
+    Every (layer, share) whose winner changed is re-timed side by side (the
+    stage-2 protocol) and its gap reported."""
+    by_id = {ld.layer_id: ld for ld in layers}
+    flips = []
+    for key in runs[0]:
+        seen = sorted({r[key] for r in runs if r[key] >= 0})
+        if len(seen) <= 1:
+            continue
+        layer, f = key
+        ld = by_id[layer]
+        sched = [cands[layer][p] for p in seen]
+        lat, st = L.measure_candidates_mask(ld.op, sched, L.ct_cu_mask(f, 0),
+                                            L.opts_from_protocol(cfg.stage2, batch=len(sched), interleave=1),
+                                            ld.x, ld.w, ld.y)
+        lat = [float(v) for v in lat]
+        flips.append({"layer": ld.op.name, "fraction": f, "positions": seen, "latency_us": lat,
+                      "gap": (max(lat) - min(lat)) / min(lat)})
+    n = len(runs[0])
+    return {"reruns": len(runs), "cells": n, "flipped_cells": len(flips),
+            "identical": n - len(flips), "max_gap": max([x["gap"] for x in flips], default=0.0), "flips": flips}
+
+
 def find_layer(name: str):
     """(op, config, layer position) of a named layer of configurations 1-5."""
     for cid in range(1, 6):
@@ -474,6 +509,9 @@ def main(argv=None) -> int:
     ap.add_argument("--fraction", type=float, default=1.0, help="CU share for --replay")
     ap.add_argument("--launches", type=int, default=200, help="back-to-back launches for --replay")
     ap.add_argument("--copy-mib", type=int, default=0, help="--replay: also run the copy kernel over this many MiB")
+    ap.add_argument("--uniform", action="store_true", help="sample the whole valid space uniformly (no family quotas)")
+    ap.add_argument("--reruns", type=int, default=1,
+                    help="run the tuning this many times with the same seed and report winner flips")
     a = ap.parse_args(argv)
     if a.replay:
         layer, fam, knobs = a.replay.split(":")
@@ -491,16 +529,35 @@ def main(argv=None) -> int:
     ops = cfg.ops[:a.layers] if a.layers else cfg.ops
     L.ct_init(0)
     layers = [make_layer(op, cfg, i) for i, op in enumerate(ops)]
-    cands = sample_all(layers, cfg)
-    report = {"config": cfg.describe(), "fractions": {}}
+    cands = sample_all(layers, cfg, uniform=a.uniform)
+    report = {"config": cfg.describe(), "sampler": "uniform" if a.uniform else "family quotas", "fractions": {}}
     winners = {}
-    for f in cfg.fractions:
-        res = tune_model_at_fraction(layers, cands, cfg, f, clients=a.clients, sharding=a.sharding)
-        report["fractions"][str(f)] = {"throughput": fraction_report(res),
-                                       "layers": [r.summary() for r in res]}
-        for r in res:
-            winners.setdefault(r.layer_id, {})[f] = r.winner
-        print("fraction %.3f: %s" % (f, json.dumps(report["fractions"][str(f)]["throughput"])), flush=True)
+    runs = []  # per rerun: {(layer, fraction): winner sample position}
+    for rerun in range(max(1, a.reruns)):
+        again = sample_all(layers, cfg, uniform=a.uniform)
+        same = all([L.schedule_tuple(s) for s in again[k]] == [L.schedule_tuple(s) for s in cands[k]] for k in cands)
+        if not same:
+            raise RuntimeError("candidate lists differ between reruns of the same seed")
+        pos = {}
+        for f in cfg.fractions:
+            res = tune_model_at_fraction(layers, cands, cfg, f, clients=a.clients, sharding=a.sharding)
+            for r in res:
+                pos[(r.layer_id, f)] = r.winner_pos
+            if rerun:
+                continue
+            report["fractions"][str(f)] = {"throughput": fraction_report(res),
+                                           "layers": [r.summary() for r in res]}
+            for r in res:
+                winners.setdefault(r.layer_id, {})[f] = r.winner
+            print("fraction %.3f: %s" % (f, json.dumps(report["fractions"][str(f)]["throughput"])), flush=True)
+        runs.append(pos)
+        if rerun:
+            print("rerun %d: %d of %d winners as in the first run" % (
+                rerun, sum(pos[k] == runs[0][k] for k in pos), len(pos)), flush=True)
+    if len(runs) > 1:
+        report["determinism"] = determinism_report(runs, layers, cands, cfg)
+        print("determinism:", json.dumps({k: v for k, v in report["determinism"].items() if k != "flips"}),
+              flush=True)
     thr = {f: report["fractions"][str(f)]["throughput"]["candidates_per_s"] for f in cfg.fractions}
     if 1.0 in thr and len(thr) > 1:
         report["throughput_vs_one_full_gpu_client"] = {str(f): thr[f] / thr[1.0] for f in cfg.fractions}

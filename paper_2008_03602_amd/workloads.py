@@ -221,8 +221,8 @@ def config(config_id: int) -> TuneConfig:
         return TuneConfig(3, "ResNet-18 cross-evaluation fp32", resnet18(1), 256,
                           (0.125, 0.25, 0.5, 0.75, 1.0), dist="normal")
     if config_id == 4:
-        return TuneConfig(4, "ResNet-50 b1 bottleneck convs, 4 clients", resnet50(1), 512, (0.25,),
-                          clients=4)
+        return TuneConfig(4, "ResNet-50 b1 bottleneck convs, 4 clients at 25% against 1 client at 100%",
+                          resnet50(1), 512, (0.25, 1.0), clients=4)
     if config_id == 5:
         return TuneConfig(5, "MobileNet-v2 b16 dw fp32 + pw bf16",
                           mobilenet_v2_depthwise(16) + mobilenet_v2_pointwise(16), 1024, (0.5, 1.0))

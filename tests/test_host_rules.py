@@ -72,6 +72,17 @@ def test_sampler_is_bit_identical_to_oracle(cfg, layer):
         assert len(set(pos)) == len(pos)
 
 
+@pytest.mark.parametrize("cfg,layer", [(2, 1), (4, 5), (5, 12)])
+def test_uniform_sampler_is_bit_identical_to_oracle(cfg, layer):
+    c = W.config(cfg)
+    op = c.ops[layer]
+    space = L.ct_valid_space(op)
+    for seed in (0, 7):
+        got = L.ct_sample_uniform(op, seed, cfg, layer, 256)
+        pos = HR.uniform_positions(len(space), 256, seed, cfg, layer)
+        assert [L.schedule_tuple(s) for s in got] == [L.schedule_tuple(space[p]) for p in pos]
+
+
 def test_family_quotas_by_hand():
     assert HR.family_quotas([5, 100], 20) == [5, 15]      # a small family hands its share on
     assert HR.family_quotas([3, 3], 10) == [3, 3]         # the whole space

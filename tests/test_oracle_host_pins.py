@@ -62,6 +62,13 @@ def pin_interleave(H):
     return got == [1, 7, 2, 6, 0, 4]
 
 
+def pin_uniform(H):
+    # the whole-space shuffle from state 0: seed = GAMMA (1 + 0) ^ 0xC0FFEE << 32 ^ 0
+    # cancels the other terms, so positions follow the size-7 worked shuffle
+    seed = 0x9E3779B97F4A7C15 ^ (0xC0FFEE << 32)
+    return H.uniform_positions(7, 5, seed, 0, 0) == [1, 2, 6, 0, 4]
+
+
 def pin_quotas(H):
     return (H.family_quotas([10, 2, 7], 12) == [5, 2, 5]      # 4+4+4, family 2 hands 2 on: 5, 2, 5
             and H.family_quotas([10, 10, 10], 10) == [4, 3, 3]
@@ -107,7 +114,7 @@ def pin_radix(H):
     return H.mixed_radix_decode([3, 4, 5], 37) == [1, 3, 2] and H.mixed_radix_encode([3, 4, 5], [1, 3, 2]) == 37
 
 
-PINS = [pin_stream, pin_shuffle, pin_interleave, pin_quotas, pin_top_t, pin_winner, pin_masks, pin_median,
+PINS = [pin_stream, pin_shuffle, pin_interleave, pin_uniform, pin_quotas, pin_top_t, pin_winner, pin_masks, pin_median,
         pin_radix]
 
 
