@@ -67,11 +67,12 @@ def kernel_source_hash(kernel: str) -> str | None:
 
 
 def _lds_ok(traced, requested) -> bool:
-    """A trace may list a dispatch's LDS as allocated, rounded up to the
-    allocation granule: accept up to 1 KiB above the bytes the launch asked for."""
-    if requested is None:
+    """A rocpd trace lists a dispatch's LDS as allocated, rounded up to the
+    allocation granule (accept up to 1 KiB above the bytes the launch asked
+    for); a csv trace reports 0 for LDS sized at launch (not a mismatch)."""
+    if requested is None or not traced:
         return True
-    return traced is not None and requested <= traced <= requested + 1024
+    return requested <= traced <= requested + 1024
 
 
 def short_name(name: str) -> str:
