@@ -71,6 +71,8 @@ struct IgF32Args {
   float inv_tiles_hw, inv_tiles_w, inv_nseg;
   int f_dm, f_dseg;            // the wave count over (filter row, segment)
   int lg_wpg, lg_wn, lg_nw;    // log2 of WM*WN, WN and the wave count
+  int swz;                     // 1: XCD-band block order (xcd_band_tile)
+  float inv_gx, inv_gxy;       // 1 / grid x, 1 / (grid x * grid y)
   int64_t ny;
 };
 
@@ -145,14 +147,27 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int wmi = wi >> a.lg_wn, wni = wi & ((1 << a.lg_wn) - 1);
   const int m_off = wmi * TM * MF, n_off = wni * TN * MF;
 
-  // block -> (image, pixel rectangle), output-channel tile, split
+  // block -> (image, pixel rectangle), output-channel tile, split. With SWZ
+  // the blocks are renumbered so that each XCD takes one contiguous band of
+  // the grid in (pixel tile, channel tile, split) order: the tiles of a band
+  // share their filter slice and the halo rows between vertically adjacent
+  // tiles in that XCD's L2, instead of every XCD fetching them again.
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  if (a.swz) {
+    const int gx = gridDim.x, gxy = gx * gridDim.y;
+    const int tb = xcd_band_tile(bx + gx * by + gxy * bz, gxy * gridDim.z);
+    bz = qdiv(tb, a.inv_gxy);
+    const int r = tb - bz * gxy;
+    by = qdiv(r, a.inv_gx);
+    bx = r - by * gx;
+  }
   const int tiles_hw = a.tiles_h * a.tiles_w;
-  const int nimg = qdiv(blockIdx.x, a.inv_tiles_hw);
-  const int trem = blockIdx.x - nimg * tiles_hw;
+  const int nimg = qdiv(bx, a.inv_tiles_hw);
+  const int trem = bx - nimg * tiles_hw;
   const int th = qdiv(trem, a.inv_tiles_w), tw = trem - th * a.tiles_w;
   const int oh0 = th * a.tph, ow0 = tw * a.tpw;
   const int ih0 = oh0 * sh - ph, iw0 = ow0 * sw - pw;
-  const int k0 = blockIdx.y * bm, sp = blockIdx.z;
+  const int k0 = by * bm, sp = bz;
   const int cl = min(a.cpc, a.C);  // channels of x in a chunk
 
   // ---- halo plan. Xs[CPCP][PP]: row hh of channel c at c*PP + hh*RW, LDS

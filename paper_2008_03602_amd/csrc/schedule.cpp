@@ -59,7 +59,8 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"tpw", 8, {7, 8, 14, 16, 28, 32, 56, 64}},
       {"cpc", 7, {1, 2, 4, 8, 16, 32, 64}},
       {"stages", 2, {1, 2}},
-      {"split", 4, {1, 2, 4, 8}}}},
+      {"split", 4, {1, 2, 4, 8}},
+      {"swz", 2, {0, 1}}}},
 };
 
 const FamilyDef* family_def(int family) {
