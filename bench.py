@@ -221,6 +221,19 @@ def main() -> int:
                                   "knobs": list(T.describe_schedule(op, lats[k][0])["knobs"].values())})
     best_layer = max(((r.op.flops() / (r.winner_lat_us * 1e-6) / 1e12 / (T.PEAK_FP32_TFLOPS * f), f, r.op.name)
                       for st in steps for f in FRACTIONS for r in st["res"][f] if r.winner is not None))
+    # where the screening time goes: per kernel family, the summed screened
+    # latency x launches per candidate (stage 1, every share, timed steps)
+    p1 = cfg.stage1
+    runs1 = p1.warmup + p1.repeats * p1.launches
+    fam_s = {}
+    for st in steps:
+        for f in FRACTIONS:
+            for r in st["res"][f]:
+                for c, lt, sc in zip(r.candidates, r.lat1, r.status1):
+                    if sc == 0 and np.isfinite(lt):
+                        k = W.FAMILY_NAMES[int(c.family)]
+                        fam_s[k] = fam_s.get(k, 0.0) + float(lt) * 1e-6 * runs1
+    tot_s = sum(fam_s.values()) or 1.0
     diag_ok = 0
     diag_n = 0
     for st in steps:
@@ -263,6 +276,7 @@ def main() -> int:
                                    for b in best_per_fraction},
         "best_layer_by_scaled_peak": {"layer": best_layer[2], "fraction": best_layer[1], "frac": best_layer[0]},
         "cross_eval_diagonal_within_3pct": [diag_ok, diag_n],
+        "stage1_device_seconds_by_family": {k: {"seconds": v, "share": v / tot_s} for k, v in sorted(fam_s.items())},
     }
     if a.report:
         rep = {"line": line, "steps": [{"batch": st["batch"],

@@ -18,8 +18,9 @@
 // the tensor (padding, a tile past the edge) gets an offset past the buffer,
 // which the hardware reads as 0. A load then needs one offset register and no
 // branch, so a thread keeps many in flight: with few threads per CU (small
-// grids) this, not the arithmetic, sets the time. The staging of an LDS chunk
-// issues kStageBatch loads per thread before the first LDS store.
+// grids) this, not the arithmetic, sets the time. An LDS chunk too deep for
+// the register prefetch is copied straight into LDS by buffer loads, every
+// element of the chunk in flight at once.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -28,8 +29,6 @@
 #include "k_util.h"
 
 namespace ct {
-
-constexpr int kStageBatch = 16;  // staging loads in flight per thread
 
 struct DirectArgs {
   int N, C, H, W, K, R, S, sh, sw, ph, pw, dh, dw;
@@ -222,33 +221,23 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
     if constexpr (LDS) {
       float* xs = smem;
       float* wsm = smem + xt;
-      // Stage the halo tile and the filter chunk: batches of kStageBatch
-      // loads per thread while the wave's first lane (its lowest element)
-      // needs a whole batch, then batches of four. Every load is issued
-      // before the batch's first LDS store; an element past the tile or
-      // outside the tensor reads 0 through the buffer's range check.
+      // Stage the halo tile and the filter chunk straight into LDS: one
+      // buffer load per element, thread t of copy j filling element
+      // j * threads + t (so a block of fewer than 64 threads works too), every
+      // copy of the chunk in flight at once, then one wait. A copy writes lane
+      // i of its wave at its LDS base + i, so each wave's base is offset by 64
+      // elements per wave before it. An element outside the tensor reads 0
+      // through the buffer's range check; lanes past the tile copy nothing.
+      const int wbase = wave_id() * 64;
       auto stage = [&](const int total, const __amdgpu_buffer_rsrc_t r, auto byte_off, float* dst) {
-        int e0 = t;
-        for (; e0 < total && __builtin_amdgcn_readfirstlane(e0) + (kStageBatch - 1) * a.threads < total;
-             e0 += kStageBatch * a.threads) {
-          float v[kStageBatch];
-#pragma unroll
-          for (int u = 0; u < kStageBatch; ++u) v[u] = bload1(r, byte_off(e0 + u * a.threads));
-#pragma unroll
-          for (int u = 0; u < kStageBatch; ++u)
-            if (e0 + u * a.threads < total) dst[e0 + u * a.threads] = v[u];
-        }
-        for (; e0 < total; e0 += 4 * a.threads) {
-          float v[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) v[u] = bload1(r, byte_off(e0 + u * a.threads));
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (e0 + u * a.threads < total) dst[e0 + u * a.threads] = v[u];
+        for (int e0 = 0; e0 < total; e0 += a.threads) {
+          const int e = e0 + t;
+          if (e < total) copy_to_lds(r, dst + e0 + wbase, byte_off(e));
         }
       };
       stage(xt, rx, [&](const int e) { return x_off(e, cc, nc); }, xs);
       stage(wt, rwt, [&](const int e) { return w_off(e, cc, nc); }, wsm);
+      wait_copies();
       __syncthreads();
       compute_lds(nc);
       __syncthreads();

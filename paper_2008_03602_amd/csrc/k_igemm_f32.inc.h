@@ -105,18 +105,6 @@ __device__ __forceinline__ f32x4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-// One wave instruction: lane i copies the word at byte offset off of r to lds[i].
-__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 4, off, 0, 0, 0);
-}
-// The same with 16 bytes per lane: lane i fills lds[4i .. 4i+3] (lds and the
-// lane's source 16-byte aligned).
-__device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, 0);
-}
-// Waits for this wave's copies to land in LDS.
-__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 template <int MF, int TM, int TN, int STAGES, int SPEC>
 __global__ void __launch_bounds__(mfma_max_threads(TM * TN * MfmaF32<MF>::ACC))

@@ -27,6 +27,20 @@ __device__ __forceinline__ float bload1(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+// One wave instruction: lane i copies the word at byte offset off of r to
+// lds[i] (an inactive lane copies nothing), without a trip through registers.
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 4, off, 0, 0, 0);
+}
+// The same with 16 bytes per lane: lane i fills lds[4i .. 4i+3] (lds and the
+// lane's source 16-byte aligned).
+__device__ __forceinline__ void copy16_to_lds(__amdgpu_buffer_rsrc_t r, float* lds, int off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds, 16, off, 0, 0, 0);
+}
+// Waits for this wave's copies to land in LDS.
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // floor(n / d) for 0 <= n < 2^22 given inv = 1/d in fp32: (n + 1/2)/d lies at
 // least 1/(2d) from an integer and the fp32 product errs by less than that.
 __device__ __forceinline__ int qdiv(int n, float inv) { return (int)(((float)n + 0.5f) * inv); }
