@@ -32,6 +32,14 @@ FAM_DEPTHWISE_F32 = 2
 FAM_IGEMM_BF16 = 3
 FAM_IGEMM_F32 = 4
 FAMILY_NAMES = {1: "direct_f32", 2: "depthwise_f32", 3: "igemm_mfma_bf16", 4: "igemm_mfma_f32"}
+# knob index of the reduction split per family (depthwise has none)
+SPLIT_KNOB = {1: 7, 3: 7, 4: 9}
+
+
+def split_of(s) -> int:
+    """How many ways schedule s splits its reduction (1: not split)."""
+    i = SPLIT_KNOB.get(int(s.family))
+    return 1 if i is None else int(s.knob[i])
 
 
 @dataclass(frozen=True)

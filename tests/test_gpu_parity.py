@@ -67,7 +67,7 @@ def _run_sample(op, n_sched, seed, dist="uniform", int_range=2, exact=False, fam
         yd.fill_(float("nan"))
         L.conv2d_run(op, s, xd, wd, yd)
         y = yd.cpu().numpy()
-        split = L.ct_launch_shape(op, s)["kernels"]
+        split = W.split_of(s)
         if exact:
             assert np.array_equal(y.astype(np.float64), ref), tag + ": not bit-exact on integer inputs"
         else:
@@ -240,7 +240,7 @@ def test_direct_staging_paths_match_oracle(op):
             note(tag)
             yd.fill_(float("nan"))
             L.conv2d_run(op, s, xd, wd, yd)
-            split = L.ct_launch_shape(op, s)["kernels"]
+            split = W.split_of(s)
             check_close(op, yd.cpu().numpy(), ref, a, tag, split=4 if split > 1 else 1)
             seen.add(cls)
             ragged += bool(op.c % s.knob[6]) and cls.startswith("prefetch")

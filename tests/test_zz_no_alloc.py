@@ -24,10 +24,10 @@ def _split_and_plain(op, per_family=2):
     space = L.ct_valid_space(op)
     out, plain = [], None
     for fam in sorted({s.family for s in space}):
-        split = [s for s in space if s.family == fam and L.ct_launch_shape(op, s)["kernels"] == 2]
+        split = [s for s in space if s.family == fam and W.split_of(s) > 1]
         out += split[::max(1, len(split) // per_family)][:per_family]
         if plain is None:
-            plain = next(s for s in space if s.family == fam and L.ct_launch_shape(op, s)["kernels"] == 1)
+            plain = next(s for s in space if s.family == fam and W.split_of(s) == 1)
     return out + [plain]
 
 
@@ -38,7 +38,7 @@ def _run_pair(op, seed):
     y2 = torch.full_like(yd, float("nan"))
     stream = torch.cuda.current_stream().cuda_stream
     scheds = _split_and_plain(op)
-    assert any(L.ct_launch_shape(op, s)["kernels"] == 2 for s in scheds)
+    assert any(W.split_of(s) > 1 for s in scheds)
     for s in scheds:
         tag = "%s %s" % (op.name, sched_str(s))
         note("noalloc " + tag)
@@ -78,7 +78,7 @@ def test_noalloc_refuses_partials_beyond_the_scratch_array():
     # the array's 2^24 (the buffers are full size all the same)
     op = W.conv("na_huge", 1, 64, 300, 64, 3, 1)
     s = next(s for s in L.ct_valid_space(op) if s.family == W.FAM_DIRECT_F32 and s.knob[7] == 4)
-    assert L.ct_launch_shape(op, s)["kernels"] == 2
+    assert W.split_of(s) > 1
     assert 4 * 64 * 300 * 300 > L.SCRATCH_FLOATS
     xd = torch.zeros(op.x_shape(), dtype=torch.float32, device="cuda")
     wd = torch.zeros(op.w_shape(), dtype=torch.float32, device="cuda")
