@@ -18,6 +18,10 @@ constexpr int kMaxLdsBytes = 160 * 1024;  // per-block LDS budget (the gfx950 wo
 constexpr int kMaxThreads = 1024;
 constexpr int kMinThreads = 32;
 constexpr int kMaxLoadsPerThread = 8;     // register staging bound of the GEMM loaders
+// fp32 MFMA family, stages 3 (four loader waves): the largest accumulator
+// tile in registers that still leaves room, two waves per SIMD, for the copy
+// plan the loaders keep across the chunk loop (no spills up to here)
+constexpr int kLoaderMaxAcc = 32;
 
 // ---- derived facts of one op ----
 struct OpX {

@@ -42,7 +42,11 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
     set_error("igemm_f32: this schedule copies 16 bytes per lane and needs 16-byte-aligned x and w");
     return -2;
   }
-  const int T = a.threads;
+  // the copy plan's strides count the waves that copy: all of them, or the
+  // four loader waves of STAGES 3 (which follow the MFMA waves)
+  a.nmw = a.wm * a.wn * a.wsp;
+  const int nw = s.knob[STAGES] == 3 ? 4 : a.threads / 64;
+  const int T = 64 * nw;
   a.pp = g.hpp; a.rw = g.hrw; a.hshift = g.hshift; a.vec_h = g.vec_h; a.vec_f = g.vec_f;
   const int vh = g.vec_h ? 4 : 1;
   const int pu = a.pp / vh, ru = a.rw / vh;
@@ -51,7 +55,6 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.inv_tpw = 1.0f / (float)a.tpw;
   a.h_dc = T / pu;
   a.h_drem = T % pu;
-  const int nw = T / 64;
   a.inv_tiles_hw = 1.0f / (float)(g.tiles_h * g.tiles_w);
   a.inv_tiles_w = 1.0f / (float)g.tiles_w;
   a.inv_nseg = 1.0f / (float)g.f_nseg;

@@ -33,8 +33,11 @@
 // B address by KSTEP channel planes. WS reduction groups split the k-steps of
 // each tap; their partial tiles are added in group order through LDS.
 // STAGES = 2 double-buffers the chunk: the copy of chunk c+1 is in flight
-// while the MFMAs of chunk c run. SPLIT > 1 spreads contiguous chunk ranges
-// over grid.z; a second kernel adds the partials in split order.
+// while the MFMAs of chunk c run. STAGES = 3 double-buffers the same way
+// with four more waves in the block (after the MFMA waves) that build the
+// copy plan and issue every copy, so the MFMA waves only compute. SPLIT > 1
+// spreads contiguous chunk ranges over grid.z; a second kernel adds the
+// partials in split order.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -70,7 +73,8 @@ struct IgF32Args {
   int h_dc, h_drem;
   float inv_tiles_hw, inv_tiles_w, inv_nseg;
   int f_dm, f_dseg;            // the wave count over (filter row, segment)
-  int lg_wpg, lg_wn, lg_nw;    // log2 of WM*WN, WN and the wave count
+  int lg_wpg, lg_wn, lg_nw;    // log2 of WM*WN, WN and the count of copying waves
+  int nmw;                     // MFMA waves (WM*WN*WS); STAGES 3 adds 4 loader waves after them
   int swz;                     // 1: XCD-band block order (xcd_band_tile)
   float inv_gx, inv_gxy;       // 1 / grid x, 1 / (grid x * grid y)
   int64_t ny;
@@ -78,7 +82,9 @@ struct IgF32Args {
 
 __host__ __device__ constexpr int ig_spec_r(int spec) { return spec == 1 || spec == 2 ? 1 : (spec == 3 || spec == 4 ? 3 : 0); }
 __host__ __device__ constexpr int ig_spec_stride(int spec) { return spec == 1 || spec == 3 ? 1 : (spec == 2 || spec == 4 ? 2 : 0); }
-// Threads per block that leave room for the accumulator tile in registers.
+// Threads per block that leave room for the accumulator tile in registers
+// (with STAGES 3, 256 MFMA threads and the 256 of the loader waves: two
+// waves per SIMD).
 __host__ __device__ constexpr int mfma_max_threads(int acc_regs) { return acc_regs <= 64 ? 512 : 256; }
 
 template <int MF>
@@ -107,7 +113,7 @@ __device__ __forceinline__ f32x4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
 
 
 template <int MF, int TM, int TN, int STAGES, int SPEC>
-__global__ void __launch_bounds__(mfma_max_threads(TM * TN * MfmaF32<MF>::ACC))
+__global__ void __launch_bounds__(STAGES == 3 ? 512 : mfma_max_threads(TM * TN * MfmaF32<MF>::ACC))
 igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ out,
                  IgF32Args a) {
   using M = MfmaF32<MF>;
@@ -128,7 +134,14 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int stage_floats = a.xs_pad + bm * lda;
 
   const int t = threadIdx.x, lane = t & 63, wave = wave_id();
-  const int nw = a.threads >> 6;
+  // The waves that copy: all of them, or with STAGES 3 the four loader waves
+  // after the MFMA waves (nw of them; this wave is number cwv among them and
+  // this thread number ct).
+  constexpr bool LOADERS = STAGES == 3;
+  const bool loader = LOADERS && wave >= a.nmw;
+  const int nw = LOADERS ? 4 : a.threads >> 6;
+  const int cwv = LOADERS ? wave - a.nmw : wave;
+  const int ct = LOADERS ? t - 64 * a.nmw : t;
   // WM, WN, WS and the wave count are powers of two: shifts, not divisions
   const int wpg = a.wm * a.wn;
   const int wg = wave >> a.lg_wpg, wi = wave & (wpg - 1);
@@ -161,14 +174,14 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   // ---- halo plan. Xs[CPCP][PP]: row hh of channel c at c*PP + hh*RW, LDS
   // column j holding input column iw0 - HSHIFT + j. Copy unit: 1 word, or 4
   // (16-byte copies: a unit is then wholly inside or wholly outside the
-  // image). Slot i of this wave copies units (i*nw + wave)*64 + lane of the
+  // image). Slot i of copying wave cwv copies units (i*nw + cwv)*64 + lane of the
   // flat array; a unit past the rows of its channel is bank padding. ----
   const int vh = a.vec_h ? 4 : 1;
   const int ru = rw / vh;
   int h_off[kHaloSlots];
-  {
+  if (!LOADERS || loader) {
     const int pu = pp / vh, rows_u = ht * ru;
-    int c = qdiv(t, a.inv_pu), rem = t - c * pu;
+    int c = qdiv(ct, a.inv_pu), rem = ct - c * pu;
 #pragma unroll
     for (int i = 0; i < kHaloSlots; ++i) {
       if (i < a.n_halo) {
@@ -185,21 +198,21 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     }
   }
   // ---- filter plan: slot j of this wave copies one segment (64 units) of row
-  // m, starting at word f_dst - m*lda; unit u = j*nw + wave enumerates
+  // m, starting at word f_dst - m*lda; unit u = j*nw + cwv enumerates
   // (m, segment) row-major. A row shorter than a segment copies only the
   // lanes it needs (a 1-word copy lands in padding of rows of at least 64
   // words); a longer row's last segment is aligned to the row end,
   // overlapping the one before it with the same data. ----
   const int vf = a.vec_f ? 4 : 1, seg_len = 64 * vf;
   const int nseg = a.f_nseg;
-  const int n_filt_w = a.n_filt_units > wave ? (a.n_filt_units - wave + nw - 1) >> a.lg_nw : 0;
+  const int n_filt_w = a.n_filt_units > cwv ? (a.n_filt_units - cwv + nw - 1) >> a.lg_nw : 0;
   // 1-word copies land in rows of at least 64 words; 16-byte copies of a row
   // shorter than a segment use only the lanes the row needs
   const bool f_lane = vf == 1 || lane * 4 < jw;
   int f_off[kFiltSlots], f_dst[kFiltSlots];
-  {
+  if (!LOADERS || loader) {
     const int dm = a.f_dm, dseg = a.f_dseg;  // nw = dm*nseg + dseg
-    int m = qdiv(wave, a.inv_nseg), seg = wave - m * nseg;
+    int m = qdiv(cwv, a.inv_nseg), seg = cwv - m * nseg;
 #pragma unroll
     for (int j = 0; j < kFiltSlots; ++j) {
       if (j < n_filt_w) {
@@ -232,11 +245,11 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     if (a.vec_h) {
 #pragma unroll
       for (int i = 0; i < kHaloSlots; ++i)
-        if (i < a.n_halo) copy16_to_lds(rx, xs + (i * nw + wave) * 256, h_off[i]);
+        if (i < a.n_halo) copy16_to_lds(rx, xs + (i * nw + cwv) * 256, h_off[i]);
     } else {
 #pragma unroll
       for (int i = 0; i < kHaloSlots; ++i)
-        if (i < a.n_halo) copy_to_lds(rx, xs + (i * nw + wave) * 64, h_off[i]);
+        if (i < a.n_halo) copy_to_lds(rx, xs + (i * nw + cwv) * 64, h_off[i]);
     }
     if (f_lane) {
       if (a.vec_f) {
@@ -355,7 +368,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     float* as = xs + a.xs_pad;
 #pragma unroll
     for (int i = 0; i < kRegCopies; ++i)
-      if (i < a.n_halo) *(f32x4*)(xs + (i * nw + wave) * 256 + lane * 4) = rh[i];
+      if (i < a.n_halo) *(f32x4*)(xs + (i * nw + cwv) * 256 + lane * 4) = rh[i];
 #pragma unroll
     for (int j = 0; j < kRegCopies; ++j)
       if (j < n_filt_w && f_lane) *(f32x4*)(as + f_dst[j] + lane * 4) = rf[j];
@@ -368,6 +381,20 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
       __syncthreads();
       compute(0);
       __syncthreads();  // the next chunk's copies overwrite this stage
+    }
+  } else if constexpr (LOADERS) {
+    // the loader waves copy, the MFMA waves compute; every wave passes every
+    // barrier
+    if (loader && ch_begin < ch_end) issue(ch_begin, 0);
+    for (int ch = ch_begin; ch < ch_end; ++ch) {
+      const int cur = (ch - ch_begin) & 1;
+      if (loader) wait_copies();
+      __syncthreads();  // chunk ch has landed; the MFMA waves are done with chunk ch-1
+      if (loader) {
+        if (ch + 1 < ch_end) issue(ch + 1, cur ^ 1);
+      } else {
+        compute(cur);
+      }
     }
   } else if (via_regs) {
     if (ch_begin < ch_end) {
@@ -403,7 +430,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
     typedef float f4 __attribute__((ext_vector_type(4)));
     f4* red = (f4*)smem;
     constexpr int Q = ACC / 4;  // 16-byte quads per accumulator tile
-    if (wg > 0) {
+    if (wg > 0 && !loader) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -419,7 +446,7 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
           }
     }
     __syncthreads();
-    if (wg > 0) return;
+    if (wg > 0) return;  // the other reduction groups and the loader waves are done
     for (int g = 1; g < a.wsp; ++g) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -435,6 +462,8 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
           }
     }
   }
+
+  if (loader) return;
 
   // Store. An accumulator's output channel splits into a wave-uniform part
   // (tile i, element e) and a lane part, so where the wave's whole channel
@@ -497,10 +526,18 @@ IgF32Fn igf32_pick_spec(int spec) {
 }
 template <int MF, int TM, int TN>
 IgF32Fn igf32_pick_stages(int stages, int spec) {
-  if constexpr (TM * TN * MfmaF32<MF>::ACC > 128)
+  constexpr int acc = TM * TN * MfmaF32<MF>::ACC;
+  if constexpr (acc > 128) {
     return nullptr;  // accumulator tiles the validator rejects: not instantiated
-  else
+  } else {
+    if (stages == 3) {
+      if constexpr (acc > kLoaderMaxAcc)
+        return nullptr;  // rejected beside loader waves: not instantiated
+      else
+        return igf32_pick_spec<MF, TM, TN, 3>(spec);
+    }
     return stages == 2 ? igf32_pick_spec<MF, TM, TN, 2>(spec) : igf32_pick_spec<MF, TM, TN, 1>(spec);
+  }
 }
 template <int MF, int TM>
 IgF32Fn igf32_pick_tn(int tn, int stages, int spec) {

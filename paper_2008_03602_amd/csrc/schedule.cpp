@@ -58,7 +58,7 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"ws", 3, {1, 2, 4}},
       {"tpw", 8, {7, 8, 14, 16, 28, 32, 56, 64}},
       {"cpc", 7, {1, 2, 4, 8, 16, 32, 64}},
-      {"stages", 2, {1, 2}},
+      {"stages", 3, {1, 2, 3}},  // 3: two stages, copies issued by four loader waves
       {"split", 4, {1, 2, 4, 8}},
       {"swz", 2, {0, 1}}}},
 };
@@ -331,8 +331,15 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   if (cpc < x.cg && x.cg % cpc) REJECT("channels per chunk do not divide C");
   const int acc_regs = tm * tn * (mf == 32 ? 16 : 4);
   if (acc_regs > 128) REJECT("accumulator tile too large");
-  const int threads = 64 * wm * wn * wsplit;
-  if (threads > mfma_thread_limit(acc_regs)) REJECT("too many threads for the accumulator tile");
+  // stages 3: the MFMA waves only compute, and four more waves build the copy
+  // plan and issue every copy into the two stages
+  const bool loaders = stages == 3;
+  const int lds_stages = std::min(stages, 2);
+  const int mfma_threads = 64 * wm * wn * wsplit;
+  if (mfma_threads > (loaders ? 256 : mfma_thread_limit(acc_regs)))
+    REJECT("too many threads for the accumulator tile");
+  if (loaders && acc_regs > kLoaderMaxAcc) REJECT("accumulator tile too large beside loader waves");
+  const int threads = mfma_threads + (loaders ? 256 : 0);
   // channels per chunk padded to whole k-steps for every reduction group
   const int kstep = mf == 32 ? 2 : 4;
   const int cpcp = (int)cdiv(cpc, kstep * wsplit) * kstep * wsplit;
@@ -352,7 +359,7 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   // channels, so the channel pitch is 16 (mod 32) and the row pitch 2 (mod 32)
   // (4 (mod 8) for 16-byte rows: a 2-way conflict); with 32x32x2 a pass reads
   // 32 rows at one k, so the row pitch is odd.
-  const int nw = threads / 64;
+  const int nw = loaders ? 4 : threads / 64;  // waves that copy
   const int cl = std::min<int>(cpc, (int)x.cg);
   const bool vec_h = o.w % 4 == 0 && (tpw * o.stride_w) % 4 == 0;
   const int hshift = vec_h ? (4 - o.pad_w % 4) % 4 : 0;
@@ -374,8 +381,8 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
     lda = mf == 16 ? lrow + ((2 - lrow) & 31) : (lrow | 1);
   }
   const int64_t units = (int64_t)cpcp * (pp / vh);
-  g->a_loads = (int)cdiv(units, 64 * nw);            // halo copies per wave per chunk
-  g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);    // filter copies per wave per chunk
+  g->a_loads = (int)cdiv(units, 64 * nw);            // halo copies per copying wave per chunk
+  g->b_loads = (int)cdiv((int64_t)bm * nseg, nw);    // filter copies per copying wave per chunk
   if (g->a_loads > 16) REJECT("too many halo copies per wave");
   if (g->b_loads > 16) REJECT("too many filter copies per wave");
   const int64_t xs_pad = (int64_t)g->a_loads * 64 * nw * vh;
@@ -387,7 +394,7 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   if (!split_ok(chunks, split, &cps)) REJECT("split leaves an empty reduction range");
   const int64_t stage_bytes = 4 * (xs_pad + (int64_t)bm * lda);
   const int64_t red_bytes = wsplit > 1 ? 4 * (int64_t)(wsplit - 1) * bm * bn : 0;
-  const int64_t lbytes = std::max(stages * stage_bytes, red_bytes);
+  const int64_t lbytes = std::max(lds_stages * stage_bytes, red_bytes);
   if (lbytes > kMaxLdsBytes) REJECT("LDS tile too large");
   g->xs_pad = (int)xs_pad;
   g->f_nseg = nseg;
