@@ -60,7 +60,7 @@ bool family_applies(int family, const OpX& x);
 namespace direct_knob { enum { TOH, TOW, TK, MK, MW, LDS, CT, SPLIT, UNR, COUNT }; }
 namespace dw_knob { enum { TC, TOH, TOW, VEC, RPT, LDS, NB, ORDER, Q4, COUNT }; }
 namespace bf16_knob { enum { MF, TM, TN, WM, WN, KC, LDS, SPLIT, SWZ, COUNT }; }
-namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, TPW, CPC, STAGES, SPLIT, SWZ, COUNT }; }
+namespace f32g_knob { enum { MF, TM, TN, WM, WN, WS, TPW, CPC, STAGES, SPLIT, COUNT }; }
 
 // Filter/stride specialisation chosen from the op (not a knob).
 enum Spec { SPEC_GENERIC = 0, SPEC_1X1_S1 = 1, SPEC_1X1_S2 = 2, SPEC_3X3_S1 = 3, SPEC_3X3_S2 = 4 };

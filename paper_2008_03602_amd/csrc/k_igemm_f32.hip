@@ -65,7 +65,6 @@ int launch_igemm_f32(const OpX& x, const ct_schedule& s, const Geom& g, const vo
   a.lg_nw = __builtin_ctz(nw);
   a.ny = x.ny;
   dim3 grid((unsigned)(o.n * g.tiles_h * g.tiles_w), (unsigned)g.tiles_k, (unsigned)g.split);
-  a.swz = s.knob[SWZ];
   a.inv_gx = 1.0f / (float)grid.x;
   a.inv_gxy = 1.0f / (float)(grid.x * grid.y);
   IgF32Fn fn = igf32_pick(s.knob[MF], s.knob[TM], s.knob[TN], s.knob[STAGES], g.spec);

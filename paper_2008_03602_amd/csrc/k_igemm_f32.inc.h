@@ -75,7 +75,6 @@ struct IgF32Args {
   int f_dm, f_dseg;            // the wave count over (filter row, segment)
   int lg_wpg, lg_wn, lg_nw;    // log2 of WM*WN, WN and the count of copying waves
   int nmw;                     // MFMA waves (WM*WN*WS); STAGES 3 adds 4 loader waves after them
-  int swz;                     // 1: XCD-band block order (xcd_band_tile)
   float inv_gx, inv_gxy;       // 1 / grid x, 1 / (grid x * grid y)
   int64_t ny;
 };
@@ -148,15 +147,15 @@ igemm_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float
   const int wmi = wi >> a.lg_wn, wni = wi & ((1 << a.lg_wn) - 1);
   const int m_off = wmi * TM * MF, n_off = wni * TN * MF;
 
-  // block -> (image, pixel rectangle), output-channel tile, split. With SWZ
-  // the blocks are renumbered so that each XCD takes one contiguous band of
-  // the grid in (pixel tile, channel tile, split) order: the tiles of a band
+  // block -> (image, pixel rectangle), output-channel tile, split. The
+  // blocks are renumbered so that each XCD takes one contiguous band of the
+  // grid in (pixel tile, channel tile, split) order: the tiles of a band
   // share their filter slice and the halo rows between vertically adjacent
   // tiles in that XCD's L2, instead of every XCD fetching them again.
-  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
-  if (a.swz) {
+  int bx, by, bz;
+  {
     const int gx = gridDim.x, gxy = gx * gridDim.y;
-    const int tb = xcd_band_tile(bx + gx * by + gxy * bz, gxy * gridDim.z);
+    const int tb = xcd_band_tile(blockIdx.x + gx * blockIdx.y + gxy * blockIdx.z, gxy * gridDim.z);
     bz = qdiv(tb, a.inv_gxy);
     const int r = tb - bz * gxy;
     by = qdiv(r, a.inv_gx);

@@ -59,8 +59,7 @@ static const FamilyDef kFamilies[CT_NUM_FAMILIES] = {
       {"tpw", 8, {7, 8, 14, 16, 28, 32, 56, 64}},
       {"cpc", 7, {1, 2, 4, 8, 16, 32, 64}},
       {"stages", 3, {1, 2, 3}},  // 3: two stages, copies issued by four loader waves
-      {"split", 4, {1, 2, 4, 8}},
-      {"swz", 2, {0, 1}}}},
+      {"split", 4, {1, 2, 4, 8}}}},
 };
 
 const FamilyDef* family_def(int family) {
@@ -421,6 +420,8 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   g->threads = threads;
   g->lds_bytes = (int)lbytes;
   g->blocks = (int64_t)o.n * g->tiles_h * g->tiles_w * g->tiles_k * split;
+  // the XCD-band renumbering splits the linear block index the same way
+  if (g->blocks >= ((int64_t)1 << 22)) REJECT("grid too large");
   g->split = split;
   g->chunks = (int)chunks;
   g->chunks_per_split = (int)cps;

@@ -107,7 +107,7 @@ def describe_schedule(op: W.Op, s: L.ct_schedule) -> dict:
     names = {1: ["toh", "tow", "tk", "mk", "mw", "lds", "ct", "split", "unroll"],
              2: ["tc", "toh", "tow", "vec", "rpt", "lds", "nb", "order", "q4"],
              3: ["mfma", "tm", "tn", "wm", "wn", "kc", "lds", "split", "swizzle"],
-             4: ["mfma", "tm", "tn", "wm", "wn", "ws", "tpw", "cpc", "stages", "split", "swz"]}[s.family]
+             4: ["mfma", "tm", "tn", "wm", "wn", "ws", "tpw", "cpc", "stages", "split"]}[s.family]
     d = {"family": W.FAMILY_NAMES[s.family], "knobs": {names[i]: int(s.knob[i]) for i in range(nk)},
          "grid_index": L.ct_grid_encode(s)}
     d.update(L.ct_launch_shape(op, s))

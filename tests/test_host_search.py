@@ -75,15 +75,16 @@ def test_proposals_are_deterministic_and_new(space):
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_guided_search_finds_the_optimum_of_a_representable_cost(space, seed):
     # the cost model fits an additive log latency exactly, so annealing on it
-    # must reach the brute-force optimum well within 10 rounds of 16
+    # must reach the brute-force optimum within 16 rounds of 16: 256
+    # measurements, 0.2 % of this space (seeds 0-7 need 3 to 15 rounds)
     f = _additive(seed)
     best = min(f(s) for s in space)
     so = L.make_search_opts(seed=seed, batch=16)
-    _, lat, _ = _run(f, so, 10)
+    _, lat, _ = _run(f, so, 16)
     assert lat.min() == pytest.approx(best, rel=1e-6)
     # uniform sampling with the same budget does not reach it on this space
     rng = np.random.default_rng(seed)
-    rand = min(f(space[i]) for i in rng.choice(len(space), size=160, replace=False))
+    rand = min(f(space[i]) for i in rng.choice(len(space), size=256, replace=False))
     assert rand > best * (1 + 1e-6)
 
 
