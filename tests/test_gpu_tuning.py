@@ -191,3 +191,31 @@ def test_full_size_resnet18_layers_verify_on_masked_streams(layer):
         yd.fill_(float("nan"))
         L.conv2d_run(op, s, xd, wd, yd)
         check_close(op, yd.cpu().numpy(), ref, a, "%s %s" % (op.name, sched_str(s)), split=8)
+
+
+def test_empty_candidate_list_and_a_layer_that_fails_verification():
+    # degenerate cases of a tuning run: no candidates to measure; a layer whose
+    # every candidate fails verification (its reference is wrong on purpose)
+    # ends with no winner while the other layer of the run tunes normally
+    cfg = W.config(2)
+    cfg.n_candidates = 8
+    cfg.top_t = 4
+    layers = [T.make_layer(op, cfg, i) for i, op in enumerate(cfg.ops[:2])]
+    note("measure an empty candidate list")
+    lat, st = L.measure_candidates_mask(layers[0].op, [], L.ct_cu_mask(0.25, 0), L.make_opts(1, 2, 2),
+                                        layers[0].x, layers[0].w, layers[0].y)
+    assert lat.size == 0 and st.size == 0
+    refs = {}
+    for ld in layers:
+        x, w = make_inputs(ld.op, cfg.dist, seed=cfg.seed, config_id=cfg.config_id, layer_id=ld.layer_id)
+        ref, _ = reference(ld.op, x, w, threads=16)
+        if ld.layer_id == 1:
+            ref = ref + 1.0  # every output off by one: no schedule can match
+        refs[ld.layer_id] = torch.from_numpy(ref.astype(np.float32)).to("cuda:0")
+    cands = T.sample_all(layers, cfg)
+    note("two layers, the second with a wrong reference, two clients at 25%")
+    res = T.tune_model_at_fraction(layers, cands, cfg, 0.25, verify_refs=refs)
+    good, bad = res[0], res[1]
+    assert good.winner_pos >= 0 and np.all(good.status1 == L.S_OK)
+    assert bad.winner_pos == -1 and np.all(bad.status1 == L.S_WRONG_ANSWER)
+    assert bad.winner_lat_us == float("inf")

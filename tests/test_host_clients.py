@@ -210,3 +210,32 @@ def test_grid_size_counts_the_valid_schedules_of_each_family(name):
     for fam in (1, 2, 3, 4):
         n = L.ct_grid_size(op, fam)
         assert n == sum(1 for s in space if s.family == fam)
+
+
+def test_empty_and_all_failed_jobs_have_no_winner_and_the_rest_finish():
+    # job 0 has no candidates; job 1 resumes a run whose candidates all timed
+    # out (every one recorded, none measured again); jobs 2 and 3 are ordinary
+    keep = T._Keep()
+    cands = L.ct_sample(OP, 0, 1, 0, 12)
+    jobs = (L.ct_tune_job * 4)()
+    T.fill_job(jobs[0], OP, 100, 1, 1, 1, [], 4, keep)
+    T.fill_job(jobs[1], OP, 101, 1, 1, 1, cands, 4, keep,
+               recorded={p: (float("inf"), L.S_TIMEOUT) for p in range(12)})
+    T.fill_job(jobs[2], OP, 102, 1, 1, 1, cands, 4, keep)
+    T.fill_job(jobs[3], OP, 103, 1, 1, 1, cands, 4, keep)
+    clients = make_clients(2)
+    owner = L.ct_test_run_clients(clients, jobs, hooks(delay_us=100))
+    assert (owner >= 0).all()
+    assert [jobs[i].rc for i in range(4)] == [0, 0, 0, 0]
+    assert jobs[0].winner_pos == -1 and jobs[0].n_top == 0 and jobs[0].winner_lat_us == float("inf")
+    assert jobs[1].winner_pos == -1 and jobs[1].n_top == 0 and jobs[1].winner_lat_us == float("inf")
+    assert jobs[2].winner_pos >= 0 and jobs[3].winner_pos >= 0
+    assert sum(c.n_measured for c in clients) == 24
+    assert all(c.rc == 0 for c in clients)
+
+
+def test_no_jobs_leaves_the_clients_idle():
+    clients = make_clients(3)
+    owner = L.ct_test_run_clients(clients, (L.ct_tune_job * 0)(), hooks())
+    assert owner.size == 0
+    assert all(c.rc == 0 and c.n_measured == 0 for c in clients)
