@@ -32,11 +32,14 @@ struct DwArgs {
   int vec_ld, vec_st;  // depthwise_q4_kernel: 16-byte input loads / output stores allowed
 };
 
+// Threads per block of the strided kernel that leave registers for its
+// outputs per thread (16 outputs need 256 VGPRs: at most 512 threads).
+__host__ __device__ constexpr int dw_max_threads(int outs) { return outs >= 16 ? 512 : 1024; }
 __host__ __device__ constexpr int dw_spec_r(int spec) { return spec == 3 || spec == 4 ? 3 : 0; }
 __host__ __device__ constexpr int dw_spec_stride(int spec) { return spec == 3 ? 1 : (spec == 4 ? 2 : 0); }
 
 template <int VEC, int RPT, bool LDS, int SPEC>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(dw_max_threads(VEC * RPT))
 depthwise_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, float* __restrict__ y,
                      DwArgs a) {
   constexpr int RC = dw_spec_r(SPEC), STC = dw_spec_stride(SPEC);

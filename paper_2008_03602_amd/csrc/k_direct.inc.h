@@ -88,7 +88,7 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
   const __amdgpu_buffer_rsrc_t rwt = make_rsrc(w, (int64_t)K * C * RS * 4);
 
   // LDS path: the block's MACs over nc staged channels
-  auto compute_lds = [&](const int nc) {
+  auto compute_lds = [&](const int nc) __attribute__((always_inline)) {
     const float* xs = smem;
     const float* wsm = smem + a.ct * a.ih_t * a.iw_t;
     const int plane = a.ih_t * a.iw_t;
@@ -143,7 +143,7 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
   // Channels of a last, partial chunk past nc stage values that the MACs
   // never read.
   const int nsx = (xt + a.threads - 1) / a.threads, nsw = (wt + a.threads - 1) / a.threads;
-  auto prefetched = [&](auto ns) {
+  auto prefetched = [&](auto ns) __attribute__((always_inline)) {
     constexpr int NS = decltype(ns)::value;
     int xo[NS], wo[NS];
 #pragma unroll
@@ -194,9 +194,10 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
   bool done = false;
   if constexpr (LDS) {
     // the deepest prefetch that leaves the MACs their registers: 16 elements
-    // per thread where the launch bound gives 256 VGPRs, else 8, or beside
-    // two unrolled channels 4 (4 accumulators) or none (8)
-    constexpr int kMaxNs = direct_max_threads(MK * MW) <= 512 ? 16
+    // per thread where the launch bound gives 256 VGPRs (8 beside 32
+    // accumulators), else 8, or beside two unrolled channels 4 (4
+    // accumulators) or none (8)
+    constexpr int kMaxNs = direct_max_threads(MK * MW) <= 512 ? (MK * MW >= 32 ? 8 : 16)
                            : UNR == 2 && MK * MW >= 8 ? 0
                            : UNR == 2 && MK * MW >= 4 ? 4 : 8;
     const int n_stage = max(nsx, nsw);
@@ -245,7 +246,7 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
       // kb: first output channel of this thread. When every wave lies inside
       // one channel group (TP a multiple of 64), kb is the same on all lanes
       // and the filter reads are scalar loads, off the vector memory path.
-      auto direct = [&](const int kb) {
+      auto direct = [&](const int kb) __attribute__((always_inline)) {
         // filter rows of this thread's channels; a channel past K reads row
         // K-1 (its sums are never stored)
         const float* wrow[MK];
@@ -268,24 +269,47 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
                 xo[r][s][j] = hok && (unsigned)gw < (unsigned)W ? (gh * W + gw) * 4 : kOob;
               }
           }
-#pragma unroll UNR
-          for (int c = 0; c < nc; ++c) {
-            const __amdgpu_buffer_rsrc_t rxc = make_rsrc(xn + (int64_t)(cc + c) * HW, (int64_t)HW * 4);
-            const int co = (cc + c) * RS;
+          // STEP channels per step: every input and filter value of the step
+          // is loaded first and the scheduling barrier keeps the MACs after
+          // them, so a step costs one memory round trip (left to itself the
+          // scheduler sinks each load next to its first use and waits for
+          // them one at a time). The channels of a step past the chunk's
+          // last one load nothing and add nothing. Each output still adds its
+          // terms channel by channel, taps in order.
+          // Two channels per step (UNR 2) only where their staged values, the
+          // input offsets and the accumulators fit the launch bound's
+          // registers (128 for 1024 threads, 256 for 512) with room to spare.
+          constexpr int T = RC * RC;
+          constexpr int kRegs = direct_max_threads(MK * MW) >= 1024 ? 128 : 256;
+          constexpr int STEP = UNR == 2 && 2 * T * (MW + MK) + T * MW + MK * MW + 24 <= kRegs ? 2 : 1;
+          for (int c = 0; c < nc; c += STEP) {
+            float xv[STEP][T][MW], wv[STEP][MK][T];
 #pragma unroll
-            for (int r = 0; r < RC; ++r)
+            for (int u = 0; u < STEP; ++u) {
+              if (u == 0 || c + u < nc) {
+                const __amdgpu_buffer_rsrc_t rxc = make_rsrc(xn + (int64_t)(cc + c + u) * HW, (int64_t)HW * 4);
+                const int co = (cc + c + u) * RS;
 #pragma unroll
-              for (int s = 0; s < RC; ++s) {
-                float xv[MW], wv[MK];
+                for (int q = 0; q < T; ++q)
 #pragma unroll
-                for (int j = 0; j < MW; ++j) xv[j] = bload1(rxc, xo[r][s][j]);
-#pragma unroll
-                for (int i = 0; i < MK; ++i) wv[i] = wrow[i][co + r * RC + s];
+                  for (int j = 0; j < MW; ++j) xv[u][q][j] = bload1(rxc, xo[q / RC][q % RC][j]);
 #pragma unroll
                 for (int i = 0; i < MK; ++i)
 #pragma unroll
-                  for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+                  for (int q = 0; q < T; ++q) wv[u][i][q] = wrow[i][co + q];
               }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < STEP; ++u) {
+              if (u > 0 && c + u >= nc) break;
+#pragma unroll
+              for (int q = 0; q < T; ++q)
+#pragma unroll
+                for (int i = 0; i < MK; ++i)
+#pragma unroll
+                  for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[u][i][q], xv[u][q][j], acc[i][j]);
+            }
           }
           return;
         }

@@ -282,7 +282,10 @@ using IgBf16Fn = void (*)(const unsigned short*, const unsigned short*, float*, 
 
 template <int MF, int TM, int TN>
 static IgBf16Fn bf_pick_lds(int lds) {
-  return lds ? igemm_bf16_kernel<MF, TM, TN, true> : igemm_bf16_kernel<MF, TM, TN, false>;
+  if constexpr (TM * TN * MfmaBf16<MF>::ACC > 128)
+    return nullptr;  // accumulator tiles the validator rejects: not instantiated
+  else
+    return lds ? igemm_bf16_kernel<MF, TM, TN, true> : igemm_bf16_kernel<MF, TM, TN, false>;
 }
 template <int MF, int TM>
 static IgBf16Fn bf_pick_tn(int tn, int lds) {
@@ -317,6 +320,10 @@ int launch_igemm_bf16(const OpX& x, const ct_schedule& s, const Geom& g, const v
   a.ny = x.ny;
   IgBf16Fn fn = s.knob[MF] == 32 ? bf_pick_tm<32>(s.knob[TM], s.knob[TN], s.knob[LDS])
                                  : bf_pick_tm<16>(s.knob[TM], s.knob[TN], s.knob[LDS]);
+  if (!fn) {
+    set_error("igemm_bf16: no kernel instance for this accumulator tile");
+    return -2;
+  }
   dim3 grid((unsigned)(g.tiles_h * g.tiles_k), (unsigned)g.split);
   float* out = g.split > 1 ? ws : (float*)y;
   hipLaunchKernelGGL(fn, grid, dim3(g.threads), g.lds_bytes, (hipStream_t)stream,

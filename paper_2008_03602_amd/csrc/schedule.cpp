@@ -245,6 +245,8 @@ static int geom_depthwise(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   const int64_t threads = (int64_t)tc * nb * (toh / rpt) * (tow / vec);
   const bool spans = tc >= o.c && nb >= o.n && toh >= x.oh && tow >= x.ow;  // as for the direct family
   if ((threads < kMinThreads && !spans) || threads > kMaxThreads) REJECT("threads per block out of range");
+  // the strided kernel's 16 outputs per thread need 256 registers: 512 threads at most
+  if (!s.knob[Q4] && vec * rpt >= 16 && threads > 512) REJECT("too many threads for 16 outputs per thread");
   g->ih_t = (int)((toh - 1) * o.stride_h + (o.r - 1) * o.dil_h + 1);
   g->iw_t = (int)((tow - 1) * o.stride_w + (o.s - 1) * o.dil_w + 1);
   int64_t lbytes = lds ? 4 * (int64_t)tc * nb * g->ih_t * g->iw_t : 0;
