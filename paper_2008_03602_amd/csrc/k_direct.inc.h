@@ -320,20 +320,37 @@ direct_f32_kernel(const float* __restrict__ x, const float* __restrict__ w, floa
           for (int r = 0; r < R; ++r) {
             const int gh = oh * sh - ph + r * dh;
             const bool hok = (unsigned)gh < (unsigned)H && oh < a.OH;
-            for (int s = 0; s < S; ++s) {
-              float xv[MW], wv[MK];
+            // the taps of a filter row go in groups of G, all of a group's
+            // loads before its MACs (one memory round trip per group, not per
+            // tap); taps past the row's end load and add nothing. G = 2 where
+            // the launch bound leaves 128 registers and a tap loads 6 or more
+            // values.
+            constexpr int G = direct_max_threads(MK * MW) >= 1024 && MK + MW >= 6 ? 2 : 4;
+            for (int s0 = 0; s0 < S; s0 += G) {
+              float xv[G][MW], wv[G][MK];
 #pragma unroll
-              for (int j = 0; j < MW; ++j) {
-                const int ow = ow0 + lc + j * a.cols;
-                const int gw = ow * sw - pw + s * dw;
-                xv[j] = bload1(rx, hok && (unsigned)gw < (unsigned)W ? (xo + gh * W + gw) * 4 : kOob);
+              for (int u = 0; u < G; ++u) {
+                if (u == 0 || s0 + u < S) {
+                  const int s = s0 + u;
+#pragma unroll
+                  for (int j = 0; j < MW; ++j) {
+                    const int ow = ow0 + lc + j * a.cols;
+                    const int gw = ow * sw - pw + s * dw;
+                    xv[u][j] = bload1(rx, hok && (unsigned)gw < (unsigned)W ? (xo + gh * W + gw) * 4 : kOob);
+                  }
+#pragma unroll
+                  for (int i = 0; i < MK; ++i) wv[u][i] = wrow[i][co + r * S + s];
+                }
               }
+              __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-              for (int i = 0; i < MK; ++i) wv[i] = wrow[i][co + r * S + s];
+              for (int u = 0; u < G; ++u) {
+                if (u > 0 && s0 + u >= S) break;
 #pragma unroll
-              for (int i = 0; i < MK; ++i)
+                for (int i = 0; i < MK; ++i)
 #pragma unroll
-                for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[i], xv[j], acc[i][j]);
+                  for (int j = 0; j < MW; ++j) acc[i][j] = fmaf(wv[u][i], xv[u][j], acc[i][j]);
+              }
             }
           }
         }
