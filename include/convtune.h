@@ -90,8 +90,24 @@ typedef struct ct_op {
 
 /* One candidate configuration (the paper's "configuration": tiles, loop
  * order, caching in LDS, unrolling, threading, matrix units -- section 2.1).
- * knob[] holds the family's knob values in its documented order; unused
- * slots are 0. Use ct_grid_decode to obtain valid encodings. */
+ * knob[] holds the family's knob values in the order below; unused slots are
+ * 0. ct_knob_values lists each knob's values and ct_grid_decode gives
+ * encodings of the grid (the validator decides which run on an op).
+ *   CT_FAM_DIRECT_F32: toh, tow (output tile), tk (output channels per
+ *     block), mk, mw (channels and columns per thread), lds (stage halo and
+ *     filter in LDS), ct (channels per chunk), split (reduction split),
+ *     unroll (channels unrolled together).
+ *   CT_FAM_DEPTHWISE_F32: tc (channels per block), toh, tow, vec, rpt
+ *     (columns and rows per thread), lds, nb (images per block), order
+ *     (block numbering: tiles fastest or channel groups fastest), q4 (4
+ *     consecutive columns per thread from 16-byte row loads).
+ *   CT_FAM_IGEMM_BF16: mfma (16 or 32: the MFMA tile), tm, tn (MFMA tiles
+ *     per wave), wm, wn (waves per block), kc (input channels per chunk),
+ *     lds (stage operands in LDS), split, swizzle (XCD-band block order).
+ *   CT_FAM_IGEMM_F32: mfma, tm, tn, wm, wn, ws (reduction groups per
+ *     block), tpw (pixel tile width), cpc (channels per chunk), stages (1:
+ *     one LDS stage; 2: two; 3: two, with four loader waves issuing every
+ *     copy), split. */
 typedef struct ct_schedule {
     int32_t family;
     int32_t knob[CT_MAX_KNOBS];
