@@ -274,14 +274,16 @@ static int ensure_err(StreamCtx* c, int slots) {
   return CT_OK;
 }
 
+// Teardown is best effort: a failing release leaves nothing else to undo, so
+// the return codes are dropped on purpose.
 static void destroy_ctx(StreamCtx* c) {
   if (c->abandoned) return;  // work may still be queued on it: leave it alone
-  if (c->stream) hipStreamSynchronize(c->stream);
-  for (hipEvent_t e : c->events) hipEventDestroy(e);
-  if (c->ws) hipFree(c->ws);
-  if (c->err) hipFree(c->err);
-  if (c->probe) hipFree(c->probe);
-  if (c->stream) hipStreamDestroy(c->stream);
+  if (c->stream) (void)hipStreamSynchronize(c->stream);
+  for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  if (c->ws) (void)hipFree(c->ws);
+  if (c->err) (void)hipFree(c->err);
+  if (c->probe) (void)hipFree(c->probe);
+  if (c->stream) (void)hipStreamDestroy(c->stream);
   delete c;
 }
 
@@ -353,14 +355,17 @@ struct EventLog {
   std::vector<int32_t> runs;   // runs enqueued since the previous event
   std::vector<int32_t> owner;  // candidate whose runs end at the event
   int pending = 0;
+  hipError_t err = hipSuccess;  // the first failed record since the last clear
   void clear() {
     ev.clear();
     runs.clear();
     owner.clear();
     pending = 0;
+    err = hipSuccess;
   }
   void record(hipEvent_t e, hipStream_t st, int who) {
-    hipEventRecord(e, st);
+    const hipError_t r = hipEventRecord(e, st);
+    if (r != hipSuccess && err == hipSuccess) err = r;
     ev.push_back(e);
     runs.push_back(pending);
     owner.push_back(who);
@@ -500,6 +505,7 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
           for (int r = 0; r < R; ++r) timed(i, i - b0, r);
     }
     int late = -1;
+    if (lg.err != hipSuccess) return hip_fail("hipEventRecord", lg.err);
     if (!lg.ev.empty()) {
       rc = wait_events(c, lg, limit_s, &late);
       if (rc == CT_E_TIMEOUT) {
@@ -533,6 +539,7 @@ static int measure_impl(const OpX& x, const ct_schedule* s, int n, StreamCtx* c,
       std::vector<unsigned> h(2 * (size_t)(b1 - b0));
       HIP_TRY(hipMemcpyAsync(h.data(), c->err, sizeof(unsigned) * h.size(), hipMemcpyDeviceToHost, st));
       lg.record(c->events[(size_t)2 * R * batch], st, -1);
+      if (lg.err != hipSuccess) return hip_fail("hipEventRecord", lg.err);
       int late2 = -1;
       rc = wait_events(c, lg, limit_s, &late2);
       if (rc == CT_E_TIMEOUT) abandon_rest(b0);
@@ -688,10 +695,10 @@ int ct_num_cus(void) {
 void ct_shutdown(void) {
   std::lock_guard<std::mutex> g(g_mu);
   if (g_device < 0 && g_pool.empty() && g_refs.empty()) return;  // nothing to release (a second call)
-  if (g_device >= 0) hipSetDevice(g_device);
+  if (g_device >= 0) (void)hipSetDevice(g_device);  // teardown: best effort
   for (StreamCtx* c : g_pool) destroy_ctx(c);
   g_pool.clear();
-  for (auto& kv : g_refs) hipFree(kv.second.d);
+  for (auto& kv : g_refs) (void)hipFree(kv.second.d);
   g_refs.clear();
   g_device = -1;
   g_num_cus = 0;
@@ -724,7 +731,7 @@ int ct_set_reference(const ct_op* op, const double* y_ref_host) {
     }
     const hipError_t e = hipMemcpy(d, h.data(), sizeof(float) * (size_t)ox.ny, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
-      hipFree(d);
+      (void)hipFree(d);
       return hip_fail("ct_set_reference: upload", e);
     }
   }
