@@ -78,13 +78,15 @@ def test_masked_slot_latency_holds_with_compute_neighbours():
 
 
 def test_guided_search_reaches_the_random_winner_on_a_layer():
-    # budget 160: the fp32 MFMA grid holds about 20k schedules of this layer,
-    # and the cost model needs a few batches of them before its proposals
-    # beat random picks
-    cfg = _cfg(160, top_t=4)
+    # budget 256 (the search study's): the fp32 MFMA grid holds about 25k
+    # schedules of this layer, and the cost model needs a few batches of them
+    # before its proposals beat random picks; its proposals follow measured,
+    # noisy latencies, so a budget near the edge fails now and then (160 came
+    # 5.4 % off once)
+    cfg = _cfg(256, top_t=4)
     layers = [T.make_layer(cfg.ops[1], cfg, 1)]
     cands = T.sample_all(layers, cfg)
-    note("guided search vs random, r18.2 at 25%, budget 160")
+    note("guided search vs random, r18.2 at 25%, budget 256")
     rep = S.search_study(layers, cands, cfg, fraction=0.25, within=0.05, patience=32)
     row = rep["layers"][0]
     print(row)
