@@ -18,6 +18,10 @@ Usage:
               dispatch; each is scaled by known bytes / counted bytes of the copy
               kernel in the same run.
 
+--sq DIR --replay FILE  SQ-counter mode: ``-f csv`` output of one ``--pmc``
+              pass of the SQ counters listed in SQ_COUNTERS over that replay;
+              writes per-dispatch, per-wave and per-MFMA figures instead.
+
 The output ends with a JSON block (``traffic``) that bench.py reads back: it
 names the kernel, its launch shape and a hash of the kernel's source files, so
 a later change to the kernel voids the figure.
@@ -399,6 +403,53 @@ def traffic_table(entries, cmds=()) -> str:
     return "\n".join(lines) + "\n"
 
 
+SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS",
+               "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_F32")
+
+
+def sq_summary(replay: dict, sq_dir: str, cmds=()) -> str:
+    """SQ counters of one replayed fp32 MFMA schedule (one --pmc pass): median
+    per dispatch, per wave and per MFMA instruction, against the MFMAs the
+    layer's FLOPs need (2048 FLOP per 16x16x4, 4096 per 32x32x2)."""
+    short = replay["kernel"]
+    med = {}
+    for c in SQ_COUNTERS:
+        vals = next((v for k, v in counter_per_dispatch(sq_dir, c).items() if short in k), [])
+        med[c] = statistics.median(vals) if vals else None
+    n_disp = len(next((v for k, v in counter_per_dispatch(sq_dir, "SQ_WAVES").items() if short in k), []))
+    knobs = ",".join(str(v) for v in replay["schedule"]["knobs"].values())
+    mfma_flops = 2048 if replay["schedule"]["knobs"].get("mfma", 16) == 16 else 4096
+    need = replay["flops"] / mfma_flops
+    lines = ["# SQ counters of `%s` on %s (knobs %s) at %g %% of the CUs" % (short, replay["layer"], knobs,
+                                                                          100 * replay["fraction"]),
+             "", "Replayed alone; medians over %d dispatches, summed over the device. Command (run from the "
+             "repository root, one pass of %d SQ counters):" % (n_disp, len(SQ_COUNTERS)), "", "```"]
+    lines += list(cmds) + ["```", "", "| counter | per dispatch | per wave | per MFMA |", "|---|---|---|---|"]
+    waves = med["SQ_WAVES"] or 0
+    mf = med["SQ_INSTS_VALU_MFMA_F32"] or 0
+    for c in SQ_COUNTERS:
+        v = med[c]
+        if v is None:
+            lines.append("| %s | - | - | - |" % c)
+            continue
+        lines.append("| %s | %.0f | %s | %s |" % (c, v, "%.1f" % (v / waves) if waves else "-",
+                                                   "%.2f" % (v / mf) if mf and c != "SQ_WAVES" else "-"))
+    if mf and waves:
+        busy = med["SQ_VALU_MFMA_BUSY_CYCLES"] or 0
+        cyc = med["SQ_WAVE_CYCLES"] or 0
+        lds = med["SQ_INSTS_LDS"] or 0
+        bc = med["SQ_LDS_BANK_CONFLICT"] or 0
+        lines += ["", "The layer needs %.0f MFMAs of %d FLOP; the kernel issues %.0f (%+.1f %%: tile padding)." % (
+            need, mfma_flops, mf, 100 * (mf / need - 1))]
+        if cyc:
+            lines.append("MFMA-busy cycles are %.1f %% of the waves' cycles (per wave %.0f of %.0f)." % (
+                100 * busy / cyc, busy / waves, cyc / waves))
+        if lds:
+            lines.append("LDS bank-conflict cycles per LDS instruction: %.2f (%.0f instructions per wave)." % (
+                bc / lds, lds / waves))
+    return "\n".join(lines) + "\n"
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--trace", default=None)
@@ -410,10 +461,16 @@ def main(argv=None) -> int:
     ap.add_argument("--write", default=None)
     ap.add_argument("--entry", action="append", default=[], metavar="REPLAY_JSON:FETCH_DIR:WRITE_DIR",
                     help="traffic-table mode: one replayed schedule and its two counter runs")
+    ap.add_argument("--sq", default=None, help="SQ-counter mode: the --pmc directory of one replay (with --replay)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args(argv)
-    if a.entry:
+    if a.sq:
+        rep = _read_json_line(a.replay, '"kernel"')
+        if rep is None:
+            ap.error("--sq needs --replay")
+        text = sq_summary(rep, a.sq, a.cmd)
+    elif a.entry:
         entries = []
         for e in a.entry:
             rj, fd, wd = e.split(":")
