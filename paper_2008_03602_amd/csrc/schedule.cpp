@@ -359,14 +359,18 @@ static int geom_igemm_f32(const OpX& x, const ct_schedule& s, Geom* g, std::stri
   // pass reads 16 filter rows at two k offsets R*S apart and 16 pixels at two
   // channels, so the channel pitch is 16 (mod 32) and the row pitch 2 (mod 32)
   // (4 (mod 8) for 16-byte rows: a 2-way conflict); with 32x32x2 a pass reads
-  // 32 rows at one k, so the row pitch is odd.
+  // 32 rows at one k, so the row pitch is odd. With 8-pixel rows (stride 1)
+  // the 16 pixels span two halo rows: a pass reads 2 channels x 2 rows x 8
+  // columns, which fall in distinct banks when the channel and row pitches
+  // are 8 and 16 (mod 32), so a row pitch of 16 takes a channel pitch of 8.
   const int nw = loaders ? 4 : threads / 64;  // waves that copy
   const int cl = std::min<int>(cpc, (int)x.cg);
   const bool vec_h = o.w % 4 == 0 && (tpw * o.stride_w) % 4 == 0;
   const int hshift = vec_h ? (4 - o.pad_w % 4) % 4 : 0;
   const int rw = vec_h ? (int)cdiv(hshift + wt, 4) * 4 : wt;
   const int rows = ht * rw;
-  const int pp = mf == 16 ? rows + ((16 - rows) & 31) : (vec_h ? (int)cdiv(rows, 4) * 4 : rows);
+  const bool two_rows = mf == 16 && tpw == 8 && o.stride_h == 1 && o.stride_w == 1 && o.dil_w == 1 && rw % 32 == 16;
+  const int pp = mf == 16 ? rows + (((two_rows ? 8 : 16) - rows) & 31) : (vec_h ? (int)cdiv(rows, 4) * 4 : rows);
   const int vh = vec_h ? 4 : 1;
   const int jw = rs * cpcp;
   const bool vec_f = mf == 16 && jw % 4 == 0 && x.kred % 4 == 0 && (cl * rs) % 4 == 0 &&

@@ -23,8 +23,9 @@ Usage:
               writes per-dispatch, per-wave and per-MFMA figures instead.
 
 The output ends with a JSON block (``traffic``) that bench.py reads back: it
-names the kernel, its launch shape and a hash of the kernel's source files, so
-a later change to the kernel voids the figure.
+names the kernel, its launch shape and a hash of the kernel's source files and
+of the schedule rules, so a later change to the kernel or its geometry voids
+the figure.
 """
 from __future__ import annotations
 
@@ -56,12 +57,13 @@ _KERNEL_SOURCES = {
 
 def kernel_source_hash(kernel: str) -> str | None:
     """sha256 over the sources of the family that `kernel` belongs to, plus the
-    shared headers; None for a kernel this library does not define."""
+    shared headers and the schedule rules that set every launch's geometry
+    (tile sizes, LDS pitches); None for a kernel this library does not define."""
     base = kernel.replace("void ", "").split("<")[0].split("(")[0].split("::")[-1]
     pats = _KERNEL_SOURCES.get(base)
     if not pats:
         return None
-    files = sorted(set(f for p in pats + ["k_util.h", "ct_internal.h"] for f in glob.glob(os.path.join(CSRC, p))))
+    files = sorted(set(f for p in pats + ["k_util.h", "ct_internal.h", "schedule.cpp"] for f in glob.glob(os.path.join(CSRC, p))))
     h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
