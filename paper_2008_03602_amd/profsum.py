@@ -50,6 +50,7 @@ PEAK_HBM_TBPS = 8.0        # MI355X HBM3E
 _KERNEL_SOURCES = {
     "direct_f32_kernel": ["k_direct*"],
     "depthwise_f32_kernel": ["k_depthwise*"],
+    "depthwise_q4_kernel": ["k_depthwise*"],
     "igemm_bf16_kernel": ["k_igemm_bf16*"],
     "igemm_f32_kernel": ["k_igemm_f32*"],
 }
