@@ -408,6 +408,13 @@ def traffic_table(entries, cmds=()) -> str:
 
 SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS",
                "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_F32")
+# The SQ counts these two in quad-cycles (4 clocks) and the MFMA-busy and
+# bank-conflict counters in clocks (rocprofiler's counter definitions);
+# the summary converts all of them to clocks.
+SQ_UNITS = {"SQ_WAVES": ("waves", 1), "SQ_WAVE_CYCLES": ("quad-cycles", 4), "SQ_INSTS_LDS": ("instructions", 1),
+            "SQ_LDS_BANK_CONFLICT": ("cycles", 1), "SQ_WAIT_INST_LDS": ("quad-cycles", 4),
+            "SQ_VALU_MFMA_BUSY_CYCLES": ("cycles", 1), "SQ_INSTS_VALU_MFMA_F32": ("instructions", 1)}
+SQ_CLOCK_GHZ = 2.4  # MI355X peak engine clock
 
 
 def sq_summary(replay: dict, sq_dir: str, cmds=()) -> str:
@@ -427,26 +434,35 @@ def sq_summary(replay: dict, sq_dir: str, cmds=()) -> str:
                                                                           100 * replay["fraction"]),
              "", "Replayed alone; medians over %d dispatches, summed over the device. Command (run from the "
              "repository root, one pass of %d SQ counters):" % (n_disp, len(SQ_COUNTERS)), "", "```"]
-    lines += list(cmds) + ["```", "", "| counter | per dispatch | per wave | per MFMA |", "|---|---|---|---|"]
+    lines += list(cmds) + ["```", "",
+                           "| counter | unit | per dispatch | per wave | per MFMA | clocks per wave |",
+                           "|---|---|---|---|---|---|"]
     waves = med["SQ_WAVES"] or 0
     mf = med["SQ_INSTS_VALU_MFMA_F32"] or 0
     for c in SQ_COUNTERS:
         v = med[c]
+        unit, clocks = SQ_UNITS[c]
         if v is None:
-            lines.append("| %s | - | - | - |" % c)
+            lines.append("| %s | %s | - | - | - | - |" % (c, unit))
             continue
-        lines.append("| %s | %.0f | %s | %s |" % (c, v, "%.1f" % (v / waves) if waves else "-",
-                                                   "%.2f" % (v / mf) if mf and c != "SQ_WAVES" else "-"))
+        lines.append("| %s | %s | %.0f | %s | %s | %s |" % (
+            c, unit, v, "%.1f" % (v / waves) if waves else "-",
+            "%.2f" % (v / mf) if mf and c != "SQ_WAVES" else "-",
+            "%.0f" % (clocks * v / waves) if waves and "cycles" in unit else "-"))
     if mf and waves:
         busy = med["SQ_VALU_MFMA_BUSY_CYCLES"] or 0
-        cyc = med["SQ_WAVE_CYCLES"] or 0
+        life = 4 * (med["SQ_WAVE_CYCLES"] or 0) / waves
         lds = med["SQ_INSTS_LDS"] or 0
         bc = med["SQ_LDS_BANK_CONFLICT"] or 0
         lines += ["", "The layer needs %.0f MFMAs of %d FLOP; the kernel issues %.0f (%+.1f %%: tile padding)." % (
             need, mfma_flops, mf, 100 * (mf / need - 1))]
-        if cyc:
-            lines.append("MFMA-busy cycles are %.1f %% of the waves' cycles (per wave %.0f of %.0f)." % (
-                100 * busy / cyc, busy / waves, cyc / waves))
+        if life:
+            # (the replay's own HIP-event latency is no check here: counter
+            # collection serialises the dispatches and inflates it)
+            lines.append("A wave lives %.0f clocks (%.2f us at %.1f GHz); its MFMAs keep the MFMA pipe busy for "
+                         "%.0f of them (%.1f %%), bank conflicts stall LDS for %.0f (%.1f %%)." % (
+                             life, life / (1e3 * SQ_CLOCK_GHZ), SQ_CLOCK_GHZ,
+                             busy / waves, 100 * busy / waves / life, bc / waves, 100 * bc / waves / life))
         if lds:
             lines.append("LDS bank-conflict cycles per LDS instruction: %.2f (%.0f instructions per wave)." % (
                 bc / lds, lds / waves))

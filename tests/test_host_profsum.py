@@ -69,3 +69,27 @@ def test_table_lookup_matches_kernel_shape_knobs_and_source_hash(tmp_path):
     h = profsum.kernel_source_hash("igemm_f32_kernel<16, 1, 1, 1, 3>")
     (prof / "table.md").write_text(text.replace(h, "0" * 16))
     assert profsum.find_traffic(str(prof), "igemm_f32_kernel<16, 1, 1, 1, 3>", shape) is None
+
+
+def test_sq_summary_converts_quad_cycles_to_clocks(tmp_path):
+    # 100 waves per dispatch: SQ_WAVE_CYCLES 2500 quad-cycles per wave = 10000
+    # clocks; 2304 MFMA-busy clocks (72 MFMAs of 32) = 23.0 % of them; 144
+    # bank-conflict clocks = 1.4 %; 2200 quad-cycles waiting on LDS = 88 clocks
+    per = {"SQ_WAVES": 100, "SQ_WAVE_CYCLES": 250000, "SQ_INSTS_LDS": 6700, "SQ_LDS_BANK_CONFLICT": 14400,
+           "SQ_WAIT_INST_LDS": 2200, "SQ_VALU_MFMA_BUSY_CYCLES": 230400, "SQ_INSTS_VALU_MFMA_F32": 7200}
+    d = tmp_path / "sq"
+    d.mkdir()
+    with open(d / "sq_counter_collection.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for disp in range(3):
+            for c, v in per.items():
+                w.writerow([disp + 1, KNAME, c, v])
+    rep = dict(_replay({"mfma": 16}), fraction=1.0, flops=7200 * 2048)
+    text = profsum.sq_summary(rep, str(d))
+    assert "| SQ_WAVE_CYCLES | quad-cycles | 250000 | 2500.0 | 34.72 | 10000 |" in text
+    assert "| SQ_WAIT_INST_LDS | quad-cycles | 2200 | 22.0 | 0.31 | 88 |" in text
+    assert "| SQ_VALU_MFMA_BUSY_CYCLES | cycles | 230400 | 2304.0 | 32.00 | 2304 |" in text
+    assert "A wave lives 10000 clocks (4.17 us at 2.4 GHz)" in text
+    assert "busy for 2304 of them (23.0 %)" in text and "stall LDS for 144 (1.4 %)" in text
+    assert "the kernel issues 7200 (+0.0 %: tile padding)" in text
