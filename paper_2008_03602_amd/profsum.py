@@ -18,8 +18,8 @@ Usage:
               dispatch; each is scaled by known bytes / counted bytes of the copy
               kernel in the same run.
 
---sq DIR --replay FILE  SQ-counter mode: ``-f csv`` output of one ``--pmc``
-              pass of the SQ counters listed in SQ_COUNTERS over that replay;
+--sq DIR --replay FILE  SQ-counter mode: ``-f csv`` output of a ``--pmc``
+              pass of SQ counters over that replay (``--sq`` once per pass);
               writes per-dispatch, per-wave and per-MFMA figures instead.
 
 The output ends with a JSON block (``traffic``) that bench.py reads back: it
@@ -408,64 +408,96 @@ def traffic_table(entries, cmds=()) -> str:
 
 SQ_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS",
                "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_F32")
-# The SQ counts these two in quad-cycles (4 clocks) and the MFMA-busy and
-# bank-conflict counters in clocks (rocprofiler's counter definitions);
-# the summary converts all of them to clocks.
+# Units of the SQ counters these summaries use, from rocprofiler's counter
+# definitions: the per-wave time counters count quad-cycles (4 clocks; a
+# wave issues at most one instruction per quad-cycle, so the ACTIVE counters
+# track the INSTS counters), the MFMA-busy and bank-conflict counters clocks.
+# The summary converts all of them to clocks.
 SQ_UNITS = {"SQ_WAVES": ("waves", 1), "SQ_WAVE_CYCLES": ("quad-cycles", 4), "SQ_INSTS_LDS": ("instructions", 1),
             "SQ_LDS_BANK_CONFLICT": ("cycles", 1), "SQ_WAIT_INST_LDS": ("quad-cycles", 4),
-            "SQ_VALU_MFMA_BUSY_CYCLES": ("cycles", 1), "SQ_INSTS_VALU_MFMA_F32": ("instructions", 1)}
+            "SQ_VALU_MFMA_BUSY_CYCLES": ("cycles", 1), "SQ_INSTS_VALU_MFMA_F32": ("instructions", 1),
+            "SQ_WAIT_ANY": ("quad-cycles", 4), "SQ_WAIT_INST_ANY": ("quad-cycles", 4),
+            "SQ_ACTIVE_INST_ANY": ("quad-cycles", 4), "SQ_ACTIVE_INST_VALU": ("quad-cycles", 4),
+            "SQ_ACTIVE_INST_LDS": ("quad-cycles", 4), "SQ_ACTIVE_INST_VMEM": ("quad-cycles", 4),
+            "SQ_ACTIVE_INST_SCA": ("quad-cycles", 4), "SQ_ACTIVE_INST_MISC": ("quad-cycles", 4),
+            "SQ_INSTS_VALU": ("instructions", 1), "SQ_INSTS_SALU": ("instructions", 1),
+            "SQ_INSTS_VMEM": ("instructions", 1)}
 SQ_CLOCK_GHZ = 2.4  # MI355X peak engine clock
 
 
-def sq_summary(replay: dict, sq_dir: str, cmds=()) -> str:
-    """SQ counters of one replayed fp32 MFMA schedule (one --pmc pass): median
-    per dispatch, per wave and per MFMA instruction, against the MFMAs the
-    layer's FLOPs need (2048 FLOP per 16x16x4, 4096 per 32x32x2)."""
+def _sq_medians(sq_dirs, short):
+    """{counter: median per dispatch} over every SQ counter found in the
+    --pmc runs (one directory per pass), and the dispatch count."""
+    med, n_disp = {}, 0
+    for d in sq_dirs:
+        names = set()
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as fh:
+                names |= {r.get("Counter_Name", "") for r in csv.DictReader(fh)}
+        for c in sorted(n for n in names if n.startswith("SQ_")):
+            vals = next((v for k, v in counter_per_dispatch(d, c).items() if short in k), [])
+            if vals:
+                med.setdefault(c, statistics.median(vals))
+                n_disp = max(n_disp, len(vals))
+    return med, n_disp
+
+
+def sq_summary(replay: dict, sq_dirs, cmds=()) -> str:
+    """SQ counters of one replayed fp32 MFMA schedule (one --pmc pass per
+    directory): median per dispatch, per wave and per MFMA instruction,
+    against the MFMAs the layer's FLOPs need (2048 FLOP per 16x16x4, 4096 per
+    32x32x2), and where the waves' time goes."""
+    if isinstance(sq_dirs, str):
+        sq_dirs = [sq_dirs]
     short = replay["kernel"]
-    med = {}
-    for c in SQ_COUNTERS:
-        vals = next((v for k, v in counter_per_dispatch(sq_dir, c).items() if short in k), [])
-        med[c] = statistics.median(vals) if vals else None
-    n_disp = len(next((v for k, v in counter_per_dispatch(sq_dir, "SQ_WAVES").items() if short in k), []))
+    med, n_disp = _sq_medians(sq_dirs, short)
+    order = [c for c in SQ_COUNTERS if c in med] + sorted(c for c in med if c not in SQ_COUNTERS and c in SQ_UNITS)
+    unknown = sorted(c for c in med if c not in SQ_UNITS)
     knobs = ",".join(str(v) for v in replay["schedule"]["knobs"].values())
     mfma_flops = 2048 if replay["schedule"]["knobs"].get("mfma", 16) == 16 else 4096
     need = replay["flops"] / mfma_flops
     lines = ["# SQ counters of `%s` on %s (knobs %s) at %g %% of the CUs" % (short, replay["layer"], knobs,
                                                                           100 * replay["fraction"]),
-             "", "Replayed alone; medians over %d dispatches, summed over the device. Command (run from the "
-             "repository root, one pass of %d SQ counters):" % (n_disp, len(SQ_COUNTERS)), "", "```"]
-    lines += list(cmds) + ["```", "",
-                           "| counter | unit | per dispatch | per wave | per MFMA | clocks per wave |",
+             "", "Replayed alone; medians over %d dispatches, summed over the device. Command%s (run from the "
+             "repository root, %d SQ counters in %d pass%s):" % (
+                 n_disp, "s" if len(cmds) > 1 else "", len(med), len(sq_dirs), "es" if len(sq_dirs) > 1 else ""),
+             "", "```"]
+    lines += list(cmds) + ["```", ""]
+    if unknown:
+        lines += ["Collected but not reported (no unit defined here): %s." % ", ".join(unknown), ""]
+    lines += ["| counter | unit | per dispatch | per wave | per MFMA | clocks per wave |",
                            "|---|---|---|---|---|---|"]
-    waves = med["SQ_WAVES"] or 0
-    mf = med["SQ_INSTS_VALU_MFMA_F32"] or 0
-    for c in SQ_COUNTERS:
+    waves = med.get("SQ_WAVES") or 0
+    mf = med.get("SQ_INSTS_VALU_MFMA_F32") or 0
+    for c in order:
         v = med[c]
         unit, clocks = SQ_UNITS[c]
-        if v is None:
-            lines.append("| %s | %s | - | - | - | - |" % (c, unit))
-            continue
         lines.append("| %s | %s | %.0f | %s | %s | %s |" % (
             c, unit, v, "%.1f" % (v / waves) if waves else "-",
             "%.2f" % (v / mf) if mf and c != "SQ_WAVES" else "-",
-            "%.0f" % (clocks * v / waves) if waves and "cycles" in unit else "-"))
+            "%.0f" % (clocks * v / waves) if waves and unit.endswith("cycles") else "-"))
+    life = 4 * med.get("SQ_WAVE_CYCLES", 0) / waves if waves else 0
     if mf and waves:
-        busy = med["SQ_VALU_MFMA_BUSY_CYCLES"] or 0
-        life = 4 * (med["SQ_WAVE_CYCLES"] or 0) / waves
-        lds = med["SQ_INSTS_LDS"] or 0
-        bc = med["SQ_LDS_BANK_CONFLICT"] or 0
         lines += ["", "The layer needs %.0f MFMAs of %d FLOP; the kernel issues %.0f (%+.1f %%: tile padding)." % (
             need, mfma_flops, mf, 100 * (mf / need - 1))]
-        if life:
+        if life and "SQ_VALU_MFMA_BUSY_CYCLES" in med:
+            busy = med["SQ_VALU_MFMA_BUSY_CYCLES"]
+            bc = med.get("SQ_LDS_BANK_CONFLICT", 0)
             # (the replay's own HIP-event latency is no check here: counter
             # collection serialises the dispatches and inflates it)
             lines.append("A wave lives %.0f clocks (%.2f us at %.1f GHz); its MFMAs keep the MFMA pipe busy for "
                          "%.0f of them (%.1f %%), bank conflicts stall LDS for %.0f (%.1f %%)." % (
                              life, life / (1e3 * SQ_CLOCK_GHZ), SQ_CLOCK_GHZ,
                              busy / waves, 100 * busy / waves / life, bc / waves, 100 * bc / waves / life))
+        lds = med.get("SQ_INSTS_LDS", 0)
         if lds:
             lines.append("LDS bank-conflict cycles per LDS instruction: %.2f (%.0f instructions per wave)." % (
-                bc / lds, lds / waves))
+                med.get("SQ_LDS_BANK_CONFLICT", 0) / lds, lds / waves))
+    if life and all(c in med for c in ("SQ_ACTIVE_INST_ANY", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY")):
+        part = [100 * 4 * med[c] / waves / life for c in ("SQ_ACTIVE_INST_ANY", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY")]
+        lines.append("Of a wave's life, %.0f %% goes to issuing instructions (SQ_ACTIVE_INST_ANY), %.0f %% to "
+                     "waiting for a dependency: memory, LDS, a barrier (SQ_WAIT_ANY), and %.0f %% to waiting "
+                     "for its turn to issue (SQ_WAIT_INST_ANY)." % tuple(part))
     return "\n".join(lines) + "\n"
 
 
@@ -480,7 +512,8 @@ def main(argv=None) -> int:
     ap.add_argument("--write", default=None)
     ap.add_argument("--entry", action="append", default=[], metavar="REPLAY_JSON:FETCH_DIR:WRITE_DIR",
                     help="traffic-table mode: one replayed schedule and its two counter runs")
-    ap.add_argument("--sq", default=None, help="SQ-counter mode: the --pmc directory of one replay (with --replay)")
+    ap.add_argument("--sq", action="append", default=[],
+                    help="SQ-counter mode: a --pmc directory of one replay (with --replay); repeat for more passes")
     ap.add_argument("--out", default=None)
     ap.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args(argv)

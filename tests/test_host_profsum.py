@@ -93,3 +93,27 @@ def test_sq_summary_converts_quad_cycles_to_clocks(tmp_path):
     assert "A wave lives 10000 clocks (4.17 us at 2.4 GHz)" in text
     assert "busy for 2304 of them (23.0 %)" in text and "stall LDS for 144 (1.4 %)" in text
     assert "the kernel issues 7200 (+0.0 %: tile padding)" in text
+
+
+def test_sq_summary_merges_passes_and_splits_a_wave_s_life(tmp_path):
+    # pass 1 as above; pass 2 adds the wave-time partition: of 2500
+    # quad-cycles per wave, 600 issuing, 1400 waiting on a dependency and 500
+    # waiting to issue (24 %, 56 %, 20 %)
+    def write(d, per):
+        d.mkdir()
+        with open(d / "sq_counter_collection.csv", "w", newline="") as fh:
+            w = csv.writer(fh)
+            w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+            for disp in range(3):
+                for c, v in per.items():
+                    w.writerow([disp + 1, KNAME, c, v])
+    write(tmp_path / "p1", {"SQ_WAVES": 100, "SQ_WAVE_CYCLES": 250000, "SQ_VALU_MFMA_BUSY_CYCLES": 230400,
+                            "SQ_INSTS_VALU_MFMA_F32": 7200})
+    write(tmp_path / "p2", {"SQ_WAVES": 100, "SQ_ACTIVE_INST_ANY": 60000, "SQ_WAIT_ANY": 140000,
+                            "SQ_WAIT_INST_ANY": 50000})
+    rep = dict(_replay({"mfma": 16}), fraction=0.25, flops=7200 * 2048)
+    text = profsum.sq_summary(rep, [str(tmp_path / "p1"), str(tmp_path / "p2")])
+    assert "7 SQ counters in 2 passes" in text
+    assert "| SQ_WAIT_ANY | quad-cycles | 140000 | 1400.0 | 19.44 | 5600 |" in text
+    assert "24 % goes to issuing instructions" in text and "56 % to waiting for a dependency" in text
+    assert "20 % to waiting for its turn to issue" in text
