@@ -18,8 +18,9 @@
 // The pitches keep MFMA operand reads free of bank conflicts (32 banks, half
 // a wave per pass): for 16x16x4 one pass reads 16 rows of A at two k offsets
 // R*S apart (odd) and 16 pixels of B at two channels, so LDA = 2 (mod 32) and
-// PP = 16 (mod 32); for 32x32x2 one pass reads 32 rows of A at one k, so LDA
-// is odd.
+// PP = 16 (mod 32), or PP = 8 (mod 32) where the 16 pixels span two halo rows
+// 16 (mod 32) apart; for 32x32x2 one pass reads 32 rows of A at one k, so LDA
+// is odd. The host sets both pitches.
 // Both are copied by buffer loads that write LDS directly, without a round
 // trip through registers: one wave instruction fills 64 consecutive LDS
 // words, lane i the i-th. The halo is copied as a flat array; the lanes'
