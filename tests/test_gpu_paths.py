@@ -7,7 +7,9 @@ the fp64 oracle, through the C ABI:
   two channels go per step (UNR 2), for 3x3 and 1x1 filters, and the
   register-bound instances that take one channel per step;
 * the direct generic-filter path (7x7, 5x3 and dilated filters), whose filter
-  rows do not divide into its tap groups.
+  rows do not divide into its tap groups;
+* fp32 MFMA schedules whose 16-pixel MFMA columns span two 8-pixel halo rows
+  16 words apart, where the halo's channel pitch is 8 (mod 32) instead of 16.
 Every case also runs on integer inputs, where any summation order is exact.
 """
 import random
@@ -21,7 +23,7 @@ from gpu_util import check_close, device_ready, make_inputs, note, reference, sc
 pytestmark = pytest.mark.gpu
 
 # knob positions (the schedule's documented order)
-F4_WS, F4_CPC, F4_STAGES = 5, 7, 8
+F4_WS, F4_TPW, F4_CPC, F4_STAGES = 5, 6, 7, 8
 D_LDS, D_CT, D_UNR, D_MK, D_MW = 5, 6, 8, 3, 4
 
 
@@ -109,3 +111,22 @@ def test_direct_generic_filter_tap_groups_match_oracle(op):
     rng = random.Random(7)
     picks = _pick(pool, lambda s: (s.knob[D_UNR], s.knob[D_MK] * s.knob[D_MW] >= 8), 2, rng)
     _run(op, picks, seed=23)
+
+
+TWO_ROW_OPS = [
+    W.conv("tr_3x3", 2, 12, 20, 24, 3, 1),                            # 3x3 fixed-filter path
+    W.Op("tr_5x5", 1, 6, 16, 16, 10, 5, 5, 1, 1, 2, 2, 1, 1, 1, 0, 0),  # generic path, rows of 16
+]
+
+
+@pytest.mark.parametrize("op", TWO_ROW_OPS, ids=lambda o: o.name)
+def test_two_row_halo_pitch_schedules_match_oracle(op):
+    # 16x16 MFMAs over 8-pixel tiles at stride 1 with 16-byte halo rows of 16
+    # words: every such schedule takes the two-row channel pitch
+    pool = [s for s in L.ct_valid_space(op) if s.family == W.FAM_IGEMM_F32 and s.knob[0] == 16
+            and s.knob[F4_TPW] == 8]
+    assert pool
+    rng = random.Random(11)
+    picks = _pick(pool, lambda s: (s.knob[F4_STAGES], s.knob[F4_WS]), 1, rng)
+    assert {s.knob[F4_STAGES] for s in picks} == {1, 2, 3}
+    _run(op, picks, seed=24)
