@@ -49,3 +49,24 @@ def test_host_units_are_clean_under_asan_and_ubsan(tmp_path):
     lines = [l for l in p.stdout.splitlines() if l.startswith("op ")]
     assert len(lines) == len(ops)
     assert all(" 0 valid" not in l for l in lines[:len(ops) - len(EDGE_OPS)])
+
+
+def test_client_machinery_is_clean_under_asan_and_ubsan(tmp_path):
+    # the client-thread driver of the race test, under the memory and
+    # undefined-behaviour sanitizers instead
+    exe = str(tmp_path / "asan_clients")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-fno-omit-frame-pointer", "-pthread", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(ROOT, "tests", "tsan_clients.cpp"), os.path.join(CSRC, "clients.cpp"),
+           os.path.join(CSRC, "schedule.cpp"), "-o", exe]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if r.returncode != 0:
+        if "sanitize" in r.stdout or "asan" in r.stdout.lower():
+            pytest.skip("g++ cannot build with the sanitizers here: " + r.stdout[-300:])
+        raise AssertionError("build failed:\n" + r.stdout[-3000:])
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1", UBSAN_OPTIONS="print_stacktrace=1")
+    p = subprocess.run([exe, str(tmp_path)], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, env=env,
+                       timeout=240)
+    assert "Sanitizer" not in p.stdout and "runtime error" not in p.stdout, p.stdout[-4000:]
+    assert p.returncode == 0, p.stdout[-4000:]
+    assert "plain: rc 0 (expected 0)" in p.stdout
