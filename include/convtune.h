@@ -506,8 +506,10 @@ int ct_test_run_clients(ct_client *clients, int n_clients, ct_tune_job *jobs, in
 int ct_test_watchdog(int n_events, const int32_t *runs, const double *done_at_s, double run_limit_s,
                      double slack_s, double drain_cap_s, int32_t *expired_event, int32_t *drained);
 
-/* The bf16 pointwise family's block renumbering (its swizzle knob), computed by
- * the same function the kernel uses: tile_of_block[b] for b < tiles. */
+/* The XCD-band block renumbering (each XCD takes one contiguous band of
+ * tiles) that the bf16 pointwise family applies under its swizzle knob and
+ * the fp32 MFMA family always, computed by the same function the kernels
+ * use: tile_of_block[b] for b < tiles. */
 int ct_test_xcd_band(int tiles, int32_t *tile_of_block);
 
 #ifdef __cplusplus
